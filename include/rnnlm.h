@@ -1,0 +1,188 @@
+/*
+ * rnnlm.h -- C ABI of a frame-wise RNNLM query scorer for AMD MI355X (gfx950).
+ *
+ * Method: Lee, Park, Kim, Lee, "Accelerating recurrent neural network language
+ * model based online speech recognition system", arXiv 1801.09866.
+ *
+ * A decoder emits, per decoding frame, LM queries = (history, next word). The
+ * library scores a whole frame per call (the paper's frame-wise batching,
+ * Sec. 4): each history vector is quantised (Sec. 3: exact, sign only, or k
+ * significant digits), keyed together with the word fed to the GRU, and
+ * de-duplicated against the frame and a GPU-resident history cache (Sec. 3,
+ * Fig. 2); each query is keyed by its history key, MaxEnt context words and
+ * target word and de-duplicated against the frame and an LM-query cache
+ * (Sec. 2.4, Fig. 1). Every history key not cached runs one GRU step
+ * (Sec. 2.1); every query not cached gets the unnormalised NCE score of its
+ * target word (Sec. 2.2) plus hashed n-gram MaxEnt weights (Sec. 2.3).
+ *
+ * Memory: every pointer argument is DEVICE memory owned by the caller unless
+ * stated otherwise. Weights are borrowed and must outlive the context. The
+ * library allocates no device memory of its own: packed weights, caches and
+ * per-frame scratch live in the caller's workspace (rnnlm_workspace_size).
+ * The context object itself is a small host allocation.
+ *
+ * Streams: `stream` arguments are hipStream_t values passed as void* (NULL =
+ * the default stream). All work is enqueued on that stream and nothing blocks
+ * the host, except rnnlm_create (which synchronises once) and rnnlm_get_stats.
+ * A context is used by one host thread at a time; calls on one context must be
+ * ordered on one stream.
+ *
+ * Errors: functions return RNNLM_OK (0) or a negative code and never throw.
+ * Host-checkable problems (null pointers, sizes above the configured maxima,
+ * bad config) return RNNLM_EINVAL before enqueueing anything. Problems only
+ * the device can see (a word id outside [0, V), a query's history index
+ * outside the frame, a non-finite history element, or |x| > 1 under decimal
+ * rounding) set bits of a sticky device flag; the offending ids are clamped so
+ * no access leaves its buffer, and that frame's outputs are unspecified.
+ * rnnlm_get_stats reports the flag and returns RNNLM_EDEVICE; afterwards
+ * rnnlm_score_frame returns RNNLM_EDEVICE until rnnlm_cache_reset clears it.
+ * rnnlm_last_error() returns a message for the calling thread's last failure.
+ */
+#ifndef RNNLM_H
+#define RNNLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { RNNLM_OK = 0, RNNLM_EINVAL = -1, RNNLM_ENOMEM = -2, RNNLM_EHIP = -3, RNNLM_EDEVICE = -4 };
+
+/* History quantisation (Sec. 3, Table 1): EXACT keeps the fp32 bits (-0 = +0);
+ * SIGN keeps only x < 0 per element; SIGDIG rounds to `qdigits` (1..3)
+ * significant decimal digits, ties away from zero, elements in [-1, 1]. */
+enum { RNNLM_Q_EXACT = 0, RNNLM_Q_SIGN = 1, RNNLM_Q_SIGDIG = 2 };
+/* Weight precision: fp32, or bf16 embedding / GRU / output weights with fp32
+ * accumulation (biases and MaxEnt weights stay fp32). */
+enum { RNNLM_F32 = 0, RNNLM_BF16 = 1 };
+/* Per-history status: key cached before this frame (HC_HIT); first of its key
+ * in the frame, GRU computed (H_REP); later copy of a key in the frame (H_DUP). */
+enum { RNNLM_H_REP = 0, RNNLM_H_DUP = 1, RNNLM_HC_HIT = 2 };
+/* Per-query status: score computed (COMPUTED); copy of an earlier query of the
+ * frame with the same key (Q_DUP); stored score returned (SCORE_HIT). */
+enum { RNNLM_Q_COMPUTED = 0, RNNLM_Q_DUP = 1, RNNLM_Q_SCORE_HIT = 2 };
+/* Sticky device error bits. */
+enum { RNNLM_DERR_WORD = 1, RNNLM_DERR_QHIST = 2, RNNLM_DERR_VALUE = 4 };
+
+typedef struct rnnlm_t rnnlm_t;   /* opaque */
+
+typedef struct {
+    int32_t V;             /* vocabulary size; word 0 is the sentence start */
+    int32_t E;             /* embedding width; multiple of 64 */
+    int32_t H;             /* GRU width; multiple of 64 */
+    int32_t L;             /* stacked GRU layers, 1 or 2 */
+    int32_t wdtype;        /* RNNLM_F32 or RNNLM_BF16 */
+    int32_t maxent_log2;   /* MaxEnt table has 2^maxent_log2 weights, 1..30 */
+    int32_t maxent_order;  /* n-gram orders 2..maxent_order are summed (1..4; 1 = none) */
+    int32_t qmode;         /* RNNLM_Q_* */
+    int32_t qdigits;       /* significant digits for RNNLM_Q_SIGDIG, 1..3 */
+    int32_t max_hist;      /* largest n_hist of any frame */
+    int32_t max_query;     /* largest n_query of any frame */
+    int32_t pad0;
+    int64_t cap_hist;      /* history-cache entries (admission stops when full) */
+    int64_t cap_query;     /* LM-query cache entries */
+    uint64_t seed;         /* seed of the history-key hash */
+} rnnlm_config;
+
+typedef struct {
+    const void *emb;       /* [V][E], wdtype */
+    const void *W_ih[2];   /* layer l: [3H][Kx], Kx = E (l = 0) or H; gate blocks (reset, update, candidate); wdtype */
+    const void *W_hh[2];   /* layer l: [3H][H], same gate blocks; wdtype */
+    const float *b_ih[2];  /* layer l: [3H] fp32; the recurrent bias is zero */
+    const void *U_out;     /* [V][H] NCE output rows, wdtype */
+    const float *b_out;    /* [V] fp32 */
+    const float *maxent;   /* [2^maxent_log2] fp32 */
+} rnnlm_weights;
+
+typedef struct {
+    int32_t n_hist;             /* history records in this frame, <= max_hist */
+    int32_t n_query;            /* queries in this frame, <= max_query */
+    const float *hist_vec;      /* [n_hist][L*H] fp32, layer-major concatenation of the layer states */
+    const int32_t *hist_words;  /* [n_hist][3]: (w-1, w-2, w-3); w-1 is the GRU input word; BOS = 0 pads */
+    const int32_t *q_hist;      /* [n_query] index into this frame's histories */
+    const int32_t *q_tgt;       /* [n_query] target word */
+} rnnlm_frame;
+
+typedef struct {
+    float *scores;      /* [n_query] fp32 log-domain scores (required when n_query > 0) */
+    float *hnew;        /* [n_hist][L*H] GRU outputs per history record (nullable) */
+    uint8_t *q_status;  /* [n_query] RNNLM_Q_* (nullable) */
+    int32_t *q_rep;     /* [n_query] lowest query index with the same key (nullable) */
+    uint8_t *h_status;  /* [n_hist] RNNLM_H_* (nullable) */
+    int32_t *h_rep;     /* [n_hist] lowest history index with the same key (nullable) */
+    uint64_t *h_hash;   /* [n_hist] 64-bit hash of the history key (nullable) */
+} rnnlm_out;
+
+typedef struct {
+    int64_t frames, queries, score_hits, query_dups, computed;
+    int64_t hists, hist_hits, hist_dups, gru_rows;
+    int64_t hist_inserted, hist_rejected, score_inserted, score_rejected;
+    int64_t hist_cache_size, score_cache_size;
+    int32_t device_error;  /* RNNLM_DERR_* bits */
+    int32_t pad;
+} rnnlm_stats;
+
+/* Bytes of device workspace a context with this config needs (256-byte
+ * aligned base required). Returns RNNLM_EINVAL for an invalid config. */
+int rnnlm_workspace_size(const rnnlm_config *cfg, size_t *bytes);
+
+/* Bind weights (device pointers, borrowed), carve up `workspace` (device,
+ * caller-owned, >= rnnlm_workspace_size bytes), pack the GRU weights, and
+ * empty both caches. Synchronises `stream` once. *out receives the context. */
+int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void *workspace,
+                 size_t ws_bytes, void *stream, rnnlm_t **out);
+
+/* Score one frame (Sec. 2.4 + Sec. 3 + Sec. 4): quantise, key and de-duplicate
+ * the histories and queries, run the GRU for uncached history keys, score the
+ * uncached queries, fill `out`, then admit the frame's new keys to the caches
+ * in ascending index while capacity lasts (a query's score is only admitted
+ * when its history key is cached). Asynchronous on `stream`. */
+int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *frame, const rnnlm_out *out, void *stream);
+
+/* Empty both caches, zero the statistics and clear the sticky device flag. */
+int rnnlm_cache_reset(rnnlm_t *ctx, void *stream);
+
+/* Full-vocabulary log normaliser (the computation NCE avoids, Sec. 2.2):
+ * logz[i] = log sum_v exp(U_out[v] . h_top[i] + b_out[v]) for i < n.
+ * h_top: [n][H] fp32 device; logz: [n] fp32 device; n <= max_hist. */
+int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *logz, void *stream);
+
+/* Copy the device statistics into *stats (host memory); synchronises `stream`.
+ * Returns RNNLM_EDEVICE if the sticky device flag is set. */
+int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *stats, void *stream);
+
+/* Test hook: quantise n fp32 elements x with the library's own kernel.
+ * codes: EXACT -> uint32[n]; SIGDIG -> uint16[n]; SIGN -> uint64[n/64]
+ * (n a multiple of 64; element i is bit i%64 of word i/64). err: one device
+ * int32 that receives RNNLM_DERR_VALUE if an element was out of domain
+ * (it is OR-ed, so clear it first). */
+int rnnlm_debug_quantize(int32_t qmode, int32_t qdigits, const float *x, int64_t n,
+                         void *codes, int32_t *err, void *stream);
+
+/* Benchmark hook: per-stage kernel timing with HIP events recorded on the
+ * frame's stream. Stages (bit i of stage_mask): 0 history keys, 1 history
+ * plan, 2 query keys, 3 query resolve, 4 query admission, 5 GRU GEMM (all
+ * layers), 6 scoring, 7 history finish, 8 normaliser GEMM, 9 normaliser
+ * combine. Only masked stages get events (each pair adds a little time
+ * between kernels). stage_mask = 0 turns timing off and releases the events.
+ * The events are host-side HIP objects; no device memory is allocated. */
+enum { RNNLM_NSTAGES = 10 };
+int rnnlm_profile(rnnlm_t *ctx, uint32_t stage_mask);
+
+/* Sum of kernel time (ms) and number of timed launches per stage since the
+ * last rnnlm_profile call; synchronises on the recorded events (host arrays
+ * of RNNLM_NSTAGES entries). */
+int rnnlm_profile_read(rnnlm_t *ctx, double *ms, int64_t *launches);
+
+/* Release the host-side context (the workspace stays the caller's). */
+void rnnlm_destroy(rnnlm_t *ctx);
+
+/* Message describing the calling thread's most recent failure ("" if none). */
+const char *rnnlm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RNNLM_H */

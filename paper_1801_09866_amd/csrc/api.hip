@@ -1,0 +1,438 @@
+// C ABI (include/rnnlm.h): configuration checks, workspace carve-up, weight
+// packing, and the per-frame launch sequence.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "common.hpp"
+#include "kernels.hpp"
+
+#define RNNLM_API extern "C" __attribute__((visibility("default")))
+
+struct rnnlm_t {
+    rnnlm_config cfg;
+    rn::Dev dev;
+    unsigned host_derr;   // sticky device error as last read by rnnlm_get_stats
+    // optional per-stage timing (rnnlm_profile)
+    uint32_t prof_mask = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_pool;   // created events
+    std::vector<int> prof_stage;                                 // stage of each used pair
+    size_t prof_used = 0;
+};
+
+namespace {
+
+// Brackets one stage's launches with an event pair when that stage is timed.
+struct StageTimer {
+    rnnlm_t *ctx;
+    hipStream_t s;
+    int stage;
+    hipEvent_t end = nullptr;
+    StageTimer(rnnlm_t *c, hipStream_t st, int stg) : ctx(c), s(st), stage(stg) {
+        if (!(ctx->prof_mask & (1u << stage))) return;
+        if (ctx->prof_used == ctx->prof_pool.size()) {
+            hipEvent_t a, b;
+            if (hipEventCreate(&a) != hipSuccess) return;
+            if (hipEventCreate(&b) != hipSuccess) { (void)hipEventDestroy(a); return; }
+            ctx->prof_pool.emplace_back(a, b);
+        }
+        auto &pr = ctx->prof_pool[ctx->prof_used++];
+        ctx->prof_stage.push_back(stage);
+        (void)hipEventRecord(pr.first, s);
+        end = pr.second;
+    }
+    ~StageTimer() {
+        if (end) (void)hipEventRecord(end, s);
+    }
+};
+
+}  // namespace
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(RNNLM_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---- exact decimal decade boundaries (smallest fp32 >= 10^-j) ----------
+typedef unsigned __int128 u128;
+
+// true iff the positive fp32 with bit pattern b is >= 10^-j
+bool ge_pow10_neg(uint32_t b, int j) {
+    const uint32_t ex = b >> 23;
+    const uint64_t M = ex ? ((b & 0x7FFFFFu) | 0x800000u) : (b & 0x7FFFFFu);
+    const int s = ex ? 150 - (int)ex : 149;   // value = M * 2^-s
+    if (s <= 0) return true;
+    if (s >= 127) return false;               // < 2^-103, far below 1e-20
+    u128 p = 1;
+    for (int i = 0; i < j; ++i) p *= 10;
+    return (u128)M * p >= ((u128)1 << s);
+}
+
+rn::DecadeTab make_decades() {
+    rn::DecadeTab t;
+    for (int j = 0; j <= 20; ++j) {
+        float approx = 1.0f;
+        for (int i = 0; i < j; ++i) approx /= 10.0f;
+        uint32_t b;
+        memcpy(&b, &approx, 4);
+        while (!ge_pow10_neg(b, j)) ++b;
+        while (b > 0 && ge_pow10_neg(b - 1, j)) --b;
+        t.lo[j] = b;
+    }
+    return t;
+}
+
+const rn::DecadeTab &decades() {
+    static rn::DecadeTab t;
+    static std::once_flag once;
+    std::call_once(once, [] { t = make_decades(); });
+    return t;
+}
+
+uint32_t pow2_at_least(long long n) {
+    uint32_t p = 16;
+    while ((long long)p < n) p <<= 1;
+    return p;
+}
+
+int code_words(const rnnlm_config &c) {
+    const int LH = c.L * c.H;
+    return c.qmode == RNNLM_Q_SIGN ? LH / 64 : (c.qmode == RNNLM_Q_SIGDIG ? LH / 4 : LH / 2);
+}
+
+int check_config(const rnnlm_config *c) {
+    if (!c) return fail(RNNLM_EINVAL, "null config");
+    if (c->V < 1 || c->V > (1 << 30)) return fail(RNNLM_EINVAL, "V out of range");
+    if (c->E < 64 || c->E % 64) return fail(RNNLM_EINVAL, "E must be a positive multiple of 64");
+    if (c->H < 64 || c->H % 64) return fail(RNNLM_EINVAL, "H must be a positive multiple of 64");
+    if (c->L < 1 || c->L > 2) return fail(RNNLM_EINVAL, "L must be 1 or 2");
+    if (c->L * c->H > rn::kMaxLH) return fail(RNNLM_EINVAL, "L*H must be <= %d", rn::kMaxLH);
+    if (c->wdtype != RNNLM_F32 && c->wdtype != RNNLM_BF16) return fail(RNNLM_EINVAL, "bad wdtype");
+    if (c->maxent_log2 < 1 || c->maxent_log2 > 30) return fail(RNNLM_EINVAL, "maxent_log2 out of range");
+    if (c->maxent_order < 1 || c->maxent_order > 4) return fail(RNNLM_EINVAL, "maxent_order must be 1..4");
+    if (c->qmode < RNNLM_Q_EXACT || c->qmode > RNNLM_Q_SIGDIG) return fail(RNNLM_EINVAL, "bad qmode");
+    if (c->qmode == RNNLM_Q_SIGDIG && (c->qdigits < 1 || c->qdigits > 3))
+        return fail(RNNLM_EINVAL, "qdigits must be 1..3");
+    if (c->max_hist < 1 || c->max_hist > (1 << 22)) return fail(RNNLM_EINVAL, "max_hist out of range");
+    if (c->max_query < 0 || c->max_query > (1 << 24)) return fail(RNNLM_EINVAL, "max_query out of range");
+    if (c->cap_hist < 0 || c->cap_hist > (1LL << 28)) return fail(RNNLM_EINVAL, "cap_hist out of range");
+    if (c->cap_query < 0 || c->cap_query > (1LL << 29)) return fail(RNNLM_EINVAL, "cap_query out of range");
+    return RNNLM_OK;
+}
+
+// Sequential carve-up of the workspace; with base == nullptr it only sizes.
+struct Carver {
+    char *base;
+    size_t off = 0;
+    template <class T>
+    T *take(size_t count) {
+        off = (off + 255) & ~(size_t)255;
+        T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+struct Extents {
+    uint32_t HI, SI, FT, QT;
+};
+
+Extents extents(const rnnlm_config &c) {
+    Extents e;
+    e.HI = pow2_at_least(2 * c.cap_hist);
+    e.SI = pow2_at_least(2 * c.cap_query);
+    e.FT = pow2_at_least(2LL * c.max_hist);
+    e.QT = pow2_at_least(2LL * (c.max_query > 0 ? c.max_query : 1));
+    return e;
+}
+
+// Lay out every device buffer; returns total bytes. Pointers are filled when
+// base != nullptr. packed[l] receives the packed weight buffer of layer l.
+size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
+    Carver cv{base};
+    const Extents x = extents(c);
+    const int LH = c.L * c.H, CW = code_words(c);
+    const size_t welem = c.wdtype == RNNLM_BF16 ? 2 : 4;
+    for (int l = 0; l < 2; ++l) {
+        packed[l] = nullptr;
+        if (l < c.L) {
+            const size_t Kx = l == 0 ? c.E : c.H;
+            packed[l] = cv.take<char>((size_t)3 * c.H * (Kx + c.H) * welem);
+        }
+    }
+    const size_t mh = c.max_hist, mq = c.max_query > 0 ? c.max_query : 1;
+    const size_t ch = c.cap_hist > 0 ? c.cap_hist : 1, cq = c.cap_query > 0 ? c.cap_query : 1;
+    d.hc_islot = cv.take<int>(x.HI);
+    d.hc_ihash = cv.take<unsigned long long>(x.HI);
+    d.hc_codes = cv.take<unsigned long long>(ch * CW);
+    d.hc_word = cv.take<int>(ch);
+    d.hc_val = cv.take<float>(ch * LH);
+    d.sc_islot = cv.take<int>(x.SI);
+    d.sc_ihash = cv.take<unsigned long long>(x.SI);
+    d.sc_key = cv.take<int4>(cq);
+    d.sc_val = cv.take<float>(cq);
+    d.ctr = cv.take<long long>(rn::C_N);
+    d.derr = cv.take<unsigned>(1);
+    d.f_codes = cv.take<unsigned long long>(mh * CW);
+    d.f_hhash = cv.take<unsigned long long>(mh);
+    d.f_words = cv.take<int>(mh * 3);
+    d.f_hcslot = cv.take<int>(mh);
+    d.f_hrep = cv.take<int>(mh);
+    d.f_hstat = cv.take<int>(mh);
+    d.f_hslot = cv.take<int>(mh);
+    d.f_ftpos = cv.take<int>(mh);
+    d.f_hptr = cv.take<unsigned long long>(mh);
+    d.f_rows = cv.take<int>(mh);
+    d.f_rowdst = cv.take<unsigned long long>(mh);
+    d.f_hval = cv.take<float>(mh * LH);
+    d.ft_hash = cv.take<unsigned long long>(x.FT);
+    d.ft_min = cv.take<int>(x.FT);
+    d.f_qkey = cv.take<int4>(mq);
+    d.f_qhist = cv.take<int>(mq);
+    d.f_qsc = cv.take<int>(mq);
+    d.f_qrep = cv.take<int>(mq);
+    d.f_qstat = cv.take<int>(mq);
+    d.f_qcand = cv.take<int>(mq);
+    d.f_qadmit = cv.take<int>(mq);
+    d.f_qtpos = cv.take<int>(mq);
+    d.qt_hash = cv.take<unsigned long long>(x.QT);
+    d.qt_min = cv.take<int>(x.QT);
+    d.ln_part = cv.take<float2>((size_t)256 * rn::lognorm_tiles(c.V));
+    return (cv.off + 255) & ~(size_t)255;
+}
+
+void reset_state(const rn::Dev &d, const Extents &x, hipStream_t s) {
+    rn::launch_fill_u32(d.hc_islot, 0xFFFFFFFFu, x.HI, s);
+    rn::launch_fill_u32(d.sc_islot, 0xFFFFFFFFu, x.SI, s);
+    rn::launch_fill_u32(d.ft_hash, 0u, 2LL * x.FT, s);
+    rn::launch_fill_u32(d.ft_min, 0x7FFFFFFFu, x.FT, s);
+    rn::launch_fill_u32(d.qt_hash, 0u, 2LL * x.QT, s);
+    rn::launch_fill_u32(d.qt_min, 0x7FFFFFFFu, x.QT, s);
+    rn::launch_fill_u32(d.ctr, 0u, 2LL * rn::C_N, s);
+    rn::launch_fill_u32(d.derr, 0u, 1, s);
+}
+
+}  // namespace
+
+RNNLM_API const char *rnnlm_last_error(void) { return g_err.c_str(); }
+
+RNNLM_API int rnnlm_workspace_size(const rnnlm_config *cfg, size_t *bytes) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!bytes) return fail(RNNLM_EINVAL, "null bytes");
+    rn::Dev d;
+    void *packed[2];
+    *bytes = layout(*cfg, nullptr, d, packed);
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void *workspace,
+                           size_t ws_bytes, void *stream, rnnlm_t **out) {
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!w || !workspace || !out) return fail(RNNLM_EINVAL, "null weights, workspace or out");
+    if (reinterpret_cast<uintptr_t>(workspace) & 255) return fail(RNNLM_EINVAL, "workspace not 256-byte aligned");
+    if (!w->emb || !w->U_out || !w->b_out) return fail(RNNLM_EINVAL, "null emb, U_out or b_out");
+    if (cfg->maxent_order >= 2 && !w->maxent) return fail(RNNLM_EINVAL, "null maxent table");
+    for (int l = 0; l < cfg->L; ++l)
+        if (!w->W_ih[l] || !w->W_hh[l] || !w->b_ih[l]) return fail(RNNLM_EINVAL, "null GRU weights of layer %d", l);
+    rn::Dev d;
+    memset(&d, 0, sizeof d);
+    void *packed[2];
+    const size_t need = layout(*cfg, reinterpret_cast<char *>(workspace), d, packed);
+    if (ws_bytes < need) return fail(RNNLM_ENOMEM, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    const Extents x = extents(*cfg);
+    d.V = cfg->V; d.E = cfg->E; d.H = cfg->H; d.L = cfg->L; d.LH = cfg->L * cfg->H;
+    d.wdtype = cfg->wdtype; d.me_log2 = cfg->maxent_log2; d.me_order = cfg->maxent_order;
+    d.qmode = cfg->qmode; d.qdigits = cfg->qmode == RNNLM_Q_SIGDIG ? cfg->qdigits : 0;
+    d.max_hist = cfg->max_hist; d.max_query = cfg->max_query; d.CW = code_words(*cfg);
+    d.cap_hist = cfg->cap_hist; d.cap_query = cfg->cap_query; d.seed = cfg->seed;
+    d.hi_mask = x.HI - 1; d.si_mask = x.SI - 1; d.ft_mask = x.FT - 1; d.qt_mask = x.QT - 1;
+    d.emb = w->emb; d.U_out = w->U_out; d.b_out = w->b_out; d.maxent = w->maxent;
+    for (int l = 0; l < 2; ++l) {
+        d.Wp[l] = packed[l];
+        d.b_ih[l] = l < cfg->L ? w->b_ih[l] : nullptr;
+    }
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    for (int l = 0; l < cfg->L; ++l) rn::launch_pack_layer(d, l, w->W_ih[l], w->W_hh[l], packed[l], s);
+    reset_state(d, x, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_create launch");
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_create sync");
+    (void)decades();
+    rnnlm_t *ctx = new (std::nothrow) rnnlm_t;
+    if (!ctx) return fail(RNNLM_ENOMEM, "host allocation failed");
+    ctx->cfg = *cfg;
+    ctx->dev = d;
+    ctx->host_derr = 0;
+    *out = ctx;
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm_out *out, void *stream) {
+    if (!ctx || !fr || !out) return fail(RNNLM_EINVAL, "null context, frame or out");
+    if (ctx->host_derr) return fail(RNNLM_EDEVICE, "sticky device error 0x%x; call rnnlm_cache_reset", ctx->host_derr);
+    const rnnlm_config &c = ctx->cfg;
+    if (fr->n_hist < 0 || fr->n_hist > c.max_hist) return fail(RNNLM_EINVAL, "n_hist %d outside [0, %d]", fr->n_hist, c.max_hist);
+    if (fr->n_query < 0 || fr->n_query > c.max_query) return fail(RNNLM_EINVAL, "n_query %d outside [0, %d]", fr->n_query, c.max_query);
+    if (fr->n_query > 0 && fr->n_hist == 0) return fail(RNNLM_EINVAL, "queries without histories");
+    if (fr->n_hist > 0 && (!fr->hist_vec || !fr->hist_words)) return fail(RNNLM_EINVAL, "null history arrays");
+    if (fr->n_query > 0 && (!fr->q_hist || !fr->q_tgt || !out->scores)) return fail(RNNLM_EINVAL, "null query arrays or scores");
+    if (fr->n_hist == 0) return RNNLM_OK;
+    if (reinterpret_cast<uintptr_t>(fr->hist_vec) & 15) return fail(RNNLM_EINVAL, "hist_vec must be 16-byte aligned");
+    if (out->hnew && (reinterpret_cast<uintptr_t>(out->hnew) & 15)) return fail(RNNLM_EINVAL, "hnew must be 16-byte aligned");
+    rn::FrameArgs f;
+    f.n_hist = fr->n_hist; f.n_query = fr->n_query;
+    f.hist_vec = fr->hist_vec; f.hist_words = fr->hist_words; f.q_hist = fr->q_hist; f.q_tgt = fr->q_tgt;
+    f.scores = out->scores; f.hnew = out->hnew; f.q_status = out->q_status; f.h_status = out->h_status;
+    f.q_rep = out->q_rep; f.h_rep = out->h_rep; f.h_hash = reinterpret_cast<rn::u64 *>(out->h_hash);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const rn::Dev &d = ctx->dev;
+    { StageTimer t(ctx, s, 0); rn::launch_hist_key(d, f, decades(), s); }
+    { StageTimer t(ctx, s, 1); rn::launch_hist_plan(d, f, s); }
+    if (f.n_query > 0) {
+        { StageTimer t(ctx, s, 2); rn::launch_query_key(d, f, s); }
+        { StageTimer t(ctx, s, 3); rn::launch_query_resolve(d, f, s); }
+        { StageTimer t(ctx, s, 4); rn::launch_query_admit(d, f, s); }
+    }
+    {
+        StageTimer t(ctx, s, 5);
+        for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, f, l, f.n_hist, s);
+    }
+    if (f.n_query > 0) { StageTimer t(ctx, s, 6); rn::launch_score(d, f, s); }
+    { StageTimer t(ctx, s, 7); rn::launch_hist_finish(d, f, s); }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_score_frame launch");
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
+    if (!ctx) return fail(RNNLM_EINVAL, "null context");
+    reset_state(ctx->dev, extents(ctx->cfg), reinterpret_cast<hipStream_t>(stream));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_cache_reset launch");
+    ctx->host_derr = 0;
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *logz, void *stream) {
+    if (!ctx) return fail(RNNLM_EINVAL, "null context");
+    if (n < 0 || n > ctx->cfg.max_hist) return fail(RNNLM_EINVAL, "n %d outside [0, %d]", n, ctx->cfg.max_hist);
+    if (n == 0) return RNNLM_OK;
+    if (!h_top || !logz) return fail(RNNLM_EINVAL, "null h_top or logz");
+    if (reinterpret_cast<uintptr_t>(h_top) & 15) return fail(RNNLM_EINVAL, "h_top must be 16-byte aligned");
+    if (ctx->cfg.wdtype != RNNLM_F32) return fail(RNNLM_EINVAL, "the normaliser needs fp32 output weights");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    for (int r0 = 0; r0 < n; r0 += 256) {
+        const int nr = n - r0 < 256 ? n - r0 : 256;
+        const float *hb = h_top + (size_t)r0 * ctx->cfg.H;
+        { StageTimer t(ctx, s, 8); rn::launch_lognorm_gemm(ctx->dev, hb, nr, s); }
+        { StageTimer t(ctx, s, 9); rn::launch_lognorm_combine(ctx->dev, nr, logz + r0, s); }
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_log_normalizer launch");
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *st, void *stream) {
+    if (!ctx || !st) return fail(RNNLM_EINVAL, "null context or stats");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    long long c[rn::C_N];
+    unsigned derr = 0;
+    hipError_t e = hipMemcpyAsync(c, ctx->dev.ctr, sizeof c, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&derr, ctx->dev.derr, sizeof derr, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_get_stats");
+    memset(st, 0, sizeof *st);
+    st->frames = c[rn::C_FRAMES]; st->queries = c[rn::C_QUERIES]; st->score_hits = c[rn::C_SCORE_HITS];
+    st->query_dups = c[rn::C_QUERY_DUPS]; st->computed = c[rn::C_COMPUTED]; st->hists = c[rn::C_HISTS];
+    st->hist_hits = c[rn::C_HIST_HITS]; st->hist_dups = c[rn::C_HIST_DUPS]; st->gru_rows = c[rn::C_GRU_ROWS];
+    st->hist_inserted = c[rn::C_HIST_INS]; st->hist_rejected = c[rn::C_HIST_REJ];
+    st->score_inserted = c[rn::C_SCORE_INS]; st->score_rejected = c[rn::C_SCORE_REJ];
+    st->hist_cache_size = c[rn::C_HC_SIZE]; st->score_cache_size = c[rn::C_SC_SIZE];
+    st->device_error = (int32_t)derr;
+    if (derr) {
+        ctx->host_derr = derr;
+        return fail(RNNLM_EDEVICE, "device error bits 0x%x", derr);
+    }
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_debug_quantize(int32_t qmode, int32_t qdigits, const float *x, int64_t n, void *codes,
+                                   int32_t *err, void *stream) {
+    if (qmode < RNNLM_Q_EXACT || qmode > RNNLM_Q_SIGDIG) return fail(RNNLM_EINVAL, "bad qmode");
+    if (qmode == RNNLM_Q_SIGDIG && (qdigits < 1 || qdigits > 3)) return fail(RNNLM_EINVAL, "qdigits must be 1..3");
+    if (n < 0 || n > (1LL << 34)) return fail(RNNLM_EINVAL, "n outside [0, 2^34]");
+    if (qmode == RNNLM_Q_SIGN && n % 64) return fail(RNNLM_EINVAL, "sign codes need n to be a multiple of 64");
+    if (n == 0) return RNNLM_OK;
+    if (!x || !codes || !err) return fail(RNNLM_EINVAL, "null pointer");
+    rn::launch_debug_quantize(x, n, qmode, qdigits, decades(), codes, reinterpret_cast<int *>(err),
+                              reinterpret_cast<hipStream_t>(stream));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_debug_quantize launch");
+    return RNNLM_OK;
+}
+
+static void profile_release(rnnlm_t *ctx) {
+    for (auto &pr : ctx->prof_pool) {
+        (void)hipEventDestroy(pr.first);
+        (void)hipEventDestroy(pr.second);
+    }
+    ctx->prof_pool.clear();
+    ctx->prof_stage.clear();
+    ctx->prof_used = 0;
+}
+
+RNNLM_API int rnnlm_profile(rnnlm_t *ctx, uint32_t stage_mask) {
+    if (!ctx) return fail(RNNLM_EINVAL, "null context");
+    if (stage_mask >> RNNLM_NSTAGES) return fail(RNNLM_EINVAL, "bad stage mask");
+    if (stage_mask == 0) {
+        profile_release(ctx);
+    } else {
+        ctx->prof_stage.clear();
+        ctx->prof_used = 0;
+    }
+    ctx->prof_mask = stage_mask;
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_profile_read(rnnlm_t *ctx, double *ms, int64_t *launches) {
+    if (!ctx || !ms || !launches) return fail(RNNLM_EINVAL, "null argument");
+    for (int i = 0; i < RNNLM_NSTAGES; ++i) { ms[i] = 0.0; launches[i] = 0; }
+    for (size_t k = 0; k < ctx->prof_used; ++k) {
+        auto &pr = ctx->prof_pool[k];
+        hipError_t e = hipEventSynchronize(pr.second);
+        if (e != hipSuccess) return hip_fail(e, "rnnlm_profile_read");
+        float t = 0.0f;
+        e = hipEventElapsedTime(&t, pr.first, pr.second);
+        if (e != hipSuccess) return hip_fail(e, "rnnlm_profile_read elapsed");
+        ms[ctx->prof_stage[k]] += t;
+        launches[ctx->prof_stage[k]] += 1;
+    }
+    return RNNLM_OK;
+}
+
+RNNLM_API void rnnlm_destroy(rnnlm_t *ctx) {
+    if (!ctx) return;
+    profile_release(ctx);
+    delete ctx;
+}

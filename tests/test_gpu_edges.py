@@ -1,0 +1,162 @@
+"""GPU edge cases against the oracle: empty and ragged frames, frames at the
+configured maxima, duplicates, tiny cache capacities, repeated frames, the
+saturated-update-gate invariant, and the sticky device error path."""
+import numpy as np
+import pytest
+import torch
+
+from harness import ATOL, RTOL, close, log
+from oracle import (H_DUP, H_REP, HC_HIT, Q_DUP, Q_SCORE_HIT, Q_SIGDIG, Q_SIGN, Oracle)
+from paper_1801_09866_amd import rnnlm as R
+from paper_1801_09866_amd.workload import F32, ModelCfg
+
+pytestmark = pytest.mark.gpu
+
+M = ModelCfg(V=5000, E=64, H=128, L=1, wdtype=F32, maxent_log2=16, maxent_order=4)
+
+
+def weights(m, rng, scale=0.05):
+    H, E = m.H, m.E
+    return {"emb": (rng.standard_normal((m.V, E)) * scale).astype(np.float32),
+            "W_ih": [(rng.standard_normal((3 * H, E if l == 0 else H)) * scale).astype(np.float32) for l in range(m.L)],
+            "W_hh": [(rng.standard_normal((3 * H, H)) * scale).astype(np.float32) for l in range(m.L)],
+            "b_ih": [(rng.standard_normal(3 * H) * scale).astype(np.float32) for l in range(m.L)],
+            "U_out": (rng.standard_normal((m.V, H)) * scale).astype(np.float32),
+            "b_out": (rng.standard_normal(m.V) * scale).astype(np.float32),
+            "maxent": (rng.standard_normal(1 << m.maxent_log2) * 0.01).astype(np.float32)}
+
+
+class Both:
+    def __init__(self, m, w, qmode, k=0, max_hist=300, max_query=3000, cap_hist=1 << 12, cap_query=1 << 14):
+        self.o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, w, qmode, k,
+                        cap_hist=cap_hist, cap_query=cap_query, seed=R.DEFAULT_SEED)
+        self.g = R.Scorer(m, w, qmode, k, max_hist=max_hist, max_query=max_query,
+                          cap_hist=cap_hist, cap_query=cap_query)
+
+    def frame(self, vec, words, qh, qt, tag=""):
+        log("  frame", tag, "n_hist", len(vec), "n_query", len(qh))
+        d = lambda a, t: torch.from_numpy(np.ascontiguousarray(a, t)).cuda()
+        out = self.g.score_frame(d(vec, np.float32), d(words, np.int32),
+                                 d(qh, np.int32) if len(qh) else None, d(qt, np.int32) if len(qt) else None)
+        res = self.o.score_frame(vec, words, qh, qt)
+        torch.cuda.synchronize()
+        n_h, n_q = len(vec), len(qh)
+        assert np.array_equal(out["h_hash"][:n_h].cpu().numpy().view(np.uint64), res.h_hash), tag
+        assert np.array_equal(out["h_status"][:n_h].cpu().numpy(), res.h_status), tag
+        assert np.array_equal(out["h_rep"][:n_h].cpu().numpy(), res.h_rep), tag
+        assert close(out["hnew"][:n_h].cpu().numpy(), res.hnew, ATOL, RTOL)[0], tag
+        if n_q:
+            assert np.array_equal(out["q_status"][:n_q].cpu().numpy(), res.q_status), tag
+            assert np.array_equal(out["q_rep"][:n_q].cpu().numpy(), res.q_rep), tag
+            assert close(out["scores"][:n_q].cpu().numpy(), res.scores, ATOL, RTOL)[0], tag
+        return out, res
+
+
+def rand_frame(rng, m, n_h, n_q, dup_every=0):
+    vec = (np.tanh(rng.standard_normal((n_h, m.L * m.H))) * 0.9).astype(np.float32)
+    words = rng.integers(0, m.V, (n_h, 3)).astype(np.int32)
+    if dup_every:
+        for i in range(dup_every, n_h, dup_every):
+            vec[i] = vec[i - dup_every]
+            words[i, 0] = words[i - dup_every, 0]
+    qh = rng.integers(0, max(n_h, 1), n_q).astype(np.int32)
+    qt = rng.integers(0, m.V, n_q).astype(np.int32)
+    return vec, words, qh, qt
+
+
+def test_ragged_sizes_empty_and_maximal():
+    rng = np.random.default_rng(0)
+    b = Both(M, weights(M, rng), Q_SIGN)
+    # nothing to do
+    out = b.g.score_frame(torch.empty((0, M.H), device="cuda"), torch.empty((0, 3), dtype=torch.int32, device="cuda"), None, None)
+    for n_h, n_q in [(1, 0), (1, 1), (63, 5), (65, 1000), (130, 0), (300, 3000), (257, 2999)]:
+        b.frame(*rand_frame(rng, M, n_h, n_q, dup_every=7), tag="%d/%d" % (n_h, n_q))
+    st = b.g.stats()
+    assert st["frames"] == 7
+
+
+def test_repeat_frame_hits_with_identical_bits():
+    rng = np.random.default_rng(1)
+    b = Both(M, weights(M, rng), Q_SIGDIG, 2)
+    f = rand_frame(rng, M, 100, 900, dup_every=5)
+    o1, r1 = b.frame(*f, tag="first")
+    s1 = o1["scores"][:900].clone()
+    o2, r2 = b.frame(*f, tag="repeat")
+    assert np.all(r2.h_status == HC_HIT) and np.all(r2.q_status == Q_SCORE_HIT)
+    assert torch.equal(o2["scores"][:900].view(torch.int32), s1.view(torch.int32))
+    assert (r1.q_status == Q_DUP).any() and (r1.h_status == H_DUP).any()
+
+
+def test_tiny_capacities_admission_order():
+    rng = np.random.default_rng(2)
+    b = Both(M, weights(M, rng), Q_SIGN, cap_hist=5, cap_query=7)
+    f = rand_frame(rng, M, 20, 60)
+    for t in range(3):
+        b.frame(*f, tag="cap %d" % t)
+    st = b.g.stats()
+    assert st["hist_cache_size"] == 5 and st["score_cache_size"] == 7
+    assert st["hist_rejected"] > 0
+
+
+def test_zero_capacities():
+    rng = np.random.default_rng(3)
+    b = Both(M, weights(M, rng), Q_SIGN, cap_hist=0, cap_query=0)
+    f = rand_frame(rng, M, 40, 200, dup_every=3)
+    b.frame(*f, tag="a")
+    b.frame(*f, tag="b")
+    assert b.g.stats()["hist_cache_size"] == 0
+
+
+def test_saturated_update_gate_keeps_history_bitwise():
+    rng = np.random.default_rng(4)
+    w = weights(M, rng)
+    w["b_ih"][0][M.H:2 * M.H] = 100.0    # z = 1 exactly in fp32 and double
+    b = Both(M, w, Q_SIGN)
+    vec, words, qh, qt = rand_frame(rng, M, 50, 10)
+    out, res = b.frame(vec, words, qh, qt, tag="z=1")
+    assert torch.equal(out["hnew"][:50].cpu(), torch.from_numpy(vec))
+
+
+def test_two_layer_fp32_and_exact_mode():
+    m = ModelCfg(V=3000, E=64, H=128, L=2, wdtype=F32, maxent_log2=12, maxent_order=3)
+    rng = np.random.default_rng(5)
+    from oracle import Q_EXACT
+    b = Both(m, weights(m, rng), Q_EXACT)
+    for t in range(3):
+        b.frame(*rand_frame(rng, m, 70, 400, dup_every=4), tag="L2 %d" % t)
+
+
+def test_device_errors_are_sticky_until_reset():
+    rng = np.random.default_rng(6)
+    g = R.Scorer(M, weights(M, rng), Q_SIGDIG, 2, max_hist=64, max_query=64)
+    vec, words, qh, qt = rand_frame(rng, M, 10, 20)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    bad_words = words.copy()
+    bad_words[3, 1] = M.V + 5
+    g.score_frame(d(vec), d(bad_words), d(qh), d(qt))
+    with pytest.raises(R.RnnlmError) as e:
+        g.stats()
+    assert e.value.code == R.EDEVICE
+    with pytest.raises(R.RnnlmError):
+        g.score_frame(d(vec), d(words), d(qh), d(qt))
+    g.reset()
+    g.score_frame(d(vec), d(words), d(qh), d(qt))
+    assert g.stats()["device_error"] == 0
+    v2 = vec.copy()
+    v2[2, 5] = 1.5          # outside [-1, 1] under decimal rounding
+    bq = qh.copy()
+    bq[0] = 99              # history index outside the frame
+    g.score_frame(d(v2), d(words), d(bq), d(qt))
+    s = g.stats(check=False)
+    assert s["device_error"] == R.DERR_VALUE | R.DERR_QHIST
+    g.reset()
+
+
+def test_host_rejects_oversized_frames():
+    rng = np.random.default_rng(7)
+    g = R.Scorer(M, weights(M, rng), Q_SIGN, max_hist=8, max_query=8)
+    vec, words, qh, qt = rand_frame(rng, M, 9, 4)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    with pytest.raises(R.RnnlmError) as e:
+        g.score_frame(d(vec), d(words), d(qh), d(qt))
+    assert e.value.code == R.EINVAL
