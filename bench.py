@@ -1,0 +1,268 @@
+"""Benchmark: frame-wise RNNLM query scoring on one MI355X.
+
+Workload (default): Large fp32 -- V=200,000, E=512, H=1024, one GRU layer,
+2^26-entry MaxEnt table with 2-, 3- and 4-gram features, 2,048 queries per
+frame from 512 fresh histories plus 30% repeated (history, word) pairs of the
+previous frame; sign-only history compression. A step is one frame through
+the whole path (quantise, hash, de-duplicate, cache probes, GRU GEMM, NCE +
+MaxEnt scoring, cache admission, h' output). Inputs are resident in HBM
+before timing starts; caches start empty at frame 0 and the first `warmup`
+frames are untimed.
+
+Prints one JSON line (see the keys below). Per-stage kernel times come from a
+replay of the same frames with HIP events around every stage, recorded by the
+library on the stream its kernels run on.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {"hbm_GBs": 8000.0, "fp32_mfma_TFs": 157.3, "bf16_mfma_TFs": 2500.0}
+METRIC = "RNNLM queries/sec (GRU+NCE+MaxEnt), H=1024 V=200k; % of MFMA/HBM roofline"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1950)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--config", default="large")
+    ap.add_argument("--qmode", default=None, help="sign | sigdig1 | sigdig2 | sigdig3 | exact")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="time budget of the oracle sample (whole frames from frame 0)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the cpu_baseline leg")
+    ap.add_argument("--no-replay", action="store_true", help="skip the per-stage timing replay")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 256 MiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def qmode_of(arg, cfg):
+    from paper_1801_09866_amd import rnnlm as R
+    if arg is None:
+        return cfg.qmodes[0]
+    if arg == "sign":
+        return (R.Q_SIGN, 0)
+    if arg == "exact":
+        return (R.Q_EXACT, 0)
+    if arg.startswith("sigdig"):
+        return (R.Q_SIGDIG, int(arg[6:]))
+    raise SystemExit("unknown qmode " + arg)
+
+
+def qmode_name(qm, k):
+    return {0: "exact", 1: "sign", 2: "sigdig%d" % k}[qm]
+
+
+def algorithmic_work(cfg, st, qm):
+    """Algorithmic FLOPs / bytes of each stage over a span with stats `st`."""
+    m = cfg.model
+    wb = 2 if m.wdtype == 1 else 4
+    LH, H, E = m.L * m.H, m.H, m.E
+    cw_bytes = {0: LH * 4, 1: LH // 8, 2: LH * 2}[qm]
+    flop_row = sum(2 * 3 * H * ((E if l == 0 else H) + H) for l in range(m.L))
+    orders = max(0, m.maxent_order - 1)
+    computed = st["computed"] + st["query_dups"]
+    per_q = H * wb + 4 + 4 * orders + 8 + 4          # row, bias, MaxEnt, ids, score
+    return {
+        "gru_gemm": ("mfma", st["gru_rows"] * flop_row),
+        "score": ("hbm", computed * per_q + st["score_hits"] * 16 + st["hists"] * H * 4),
+        "hist_key": ("hbm", st["hists"] * (LH * 4 + 12 + cw_bytes + 8) + st["hist_hits"] * cw_bytes),
+        "hist_finish": ("hbm", 2 * st["hists"] * LH * 4 + st["hist_inserted"] * cw_bytes),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(the design for sharding is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_1801_09866_amd import rnnlm as R
+    from paper_1801_09866_amd.workload import CONFIGS, make_workload
+
+    cfg = CONFIGS[args.config]
+    qm, qk = qmode_of(args.qmode, cfg)
+    n_frames = min(cfg.frames, args.warmup + args.steps)
+    W, K = min(args.warmup, n_frames - 1), n_frames - min(args.warmup, n_frames - 1)
+    t0 = time.time()
+    wl = make_workload(args.config, n_frames=n_frames)
+    log("workload %s generated in %.1fs: %d frames" % (args.config, time.time() - t0, n_frames))
+    m = cfg.model
+    LH = m.L * m.H
+    dev = torch.device("cuda:0")
+    sc = R.Scorer(m, wl.weights, qm, qk, max_hist=cfg.max_hist, max_query=max(cfg.queries, 1),
+                  cap_hist=cfg.cap_hist, cap_query=cfg.cap_query, device="cuda:0")
+
+    # ---- inputs resident in HBM: all frames, back to back ----------------
+    pool = torch.from_numpy(wl.pool.vec).to(dev)
+    nh = np.array([f.n_hist for f in wl.frames])
+    nq = np.array([f.n_query for f in wl.frames])
+    ho = np.concatenate([[0], np.cumsum(nh)])
+    qo = np.concatenate([[0], np.cumsum(nq)])
+    hv = pool.index_select(0, torch.from_numpy(np.concatenate([f.pool_idx for f in wl.frames])).to(dev))
+    hw = torch.from_numpy(np.concatenate([f.hist_words for f in wl.frames]).astype(np.int32)).to(dev)
+    qh = torch.from_numpy(np.concatenate([f.q_hist for f in wl.frames]).astype(np.int32)).to(dev)
+    qt = torch.from_numpy(np.concatenate([f.q_tgt for f in wl.frames]).astype(np.int32)).to(dev)
+    scores = torch.empty(max(int(qo[-1]), 1), dtype=torch.float32, device=dev)
+    hnew = torch.empty((int(ho[-1]), LH), dtype=torch.float32, device=dev)
+    del pool
+    fsz, hsz = hv.element_size() * LH, 4
+    frames, outs = [], []
+    for i in range(n_frames):
+        frames.append(R.Frame(int(nh[i]), int(nq[i]), hv.data_ptr() + int(ho[i]) * fsz,
+                              hw.data_ptr() + int(ho[i]) * 12, qh.data_ptr() + int(qo[i]) * 4,
+                              qt.data_ptr() + int(qo[i]) * 4))
+        outs.append(R.Out(scores.data_ptr() + int(qo[i]) * 4, hnew.data_ptr() + int(ho[i]) * LH * hsz,
+                          None, None, None, None, None))
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    L = R.load()
+    ctx = sc.ctx
+
+    def run(lo, hi):
+        for i in range(lo, hi):
+            rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[i]), ctypes.byref(outs[i]), sp)
+            if rc:
+                raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
+
+    # ---- warmup + timed region -------------------------------------------
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    st0 = sc.stats()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    ev0.record(stream)
+    run(W, n_frames)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    gpu_ms = ev0.elapsed_time(ev1)
+    st1 = sc.stats()
+    span = {k: st1[k] - st0[k] for k in st1 if k not in ("hist_cache_size", "score_cache_size", "device_error")}
+    secs = gpu_ms / 1e3
+    queries = int(qo[n_frames] - qo[W])
+    value = queries / secs
+    log("timed %d frames: %.3f ms GPU (%.3f ms wall), %.0f queries/s" % (K, gpu_ms, wall * 1e3, value))
+
+    # ---- per-stage kernel times: replay the same frames with events ------
+    stages, roofline = {}, None
+    if not args.no_replay:
+        sc.reset()
+        run(0, W)
+        sc.profile(R.STAGES[:8])
+        run(W, n_frames)
+        torch.cuda.synchronize()
+        prof = sc.profile_read()
+        sc.profile(())
+        work = algorithmic_work(cfg, span, qm)
+        for name, (ms, launches) in prof.items():
+            entry = {"ms_total": round(ms, 4), "launches": launches, "us_per_launch": round(1e3 * ms / launches, 2)}
+            if name in work:
+                bound, amount = work[name]
+                if bound == "mfma":
+                    peak = PEAK["bf16_mfma_TFs"] if m.wdtype == 1 else PEAK["fp32_mfma_TFs"]
+                    ach = amount / (ms / 1e3) / 1e12 if ms > 0 else 0.0
+                    entry.update(bound="mfma", achieved=round(ach, 2), peak=peak, unit="TFLOP/s",
+                                 frac=round(ach / peak, 4), algorithmic=amount)
+                else:
+                    ach = amount / (ms / 1e3) / 1e9 if ms > 0 else 0.0
+                    entry.update(bound="hbm", achieved=round(ach, 1), peak=PEAK["hbm_GBs"], unit="GB/s",
+                                 frac=round(ach / PEAK["hbm_GBs"], 4), algorithmic=amount)
+            stages[name] = entry
+        dom = max((n for n in stages if "bound" in stages[n]), key=lambda n: stages[n]["ms_total"])
+        e = stages[dom]
+        roofline = {"kernel": dom, "bound": e["bound"], "achieved": e["achieved"], "peak": e["peak"],
+                    "unit": e["unit"], "frac": e["frac"], "traffic": None,
+                    "us_per_launch": e["us_per_launch"]}
+        log("stages:", json.dumps(stages))
+
+    if args.copy_calibration:
+        a = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    # ---- cpu baseline: the oracle on a bounded prefix of the same frames --
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(args, wl, qm, qk, sc, run, frames)
+
+    hit = lambda a, b: round(a / b, 4) if b else None
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(gpu_ms / K, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16-weights/f32-accumulate" if m.wdtype == 1 else "f32", "data": "synthetic",
+        "config": {"workload": "%s_%s: V=%d E=%d H=%d L=%d MaxEnt 2^%d orders 2..%d, %d queries/frame"
+                               % (cfg.name, qmode_name(qm, qk), m.V, m.E, m.H, m.L, m.maxent_log2,
+                                  m.maxent_order, cfg.queries),
+                   "frames_timed": K, "queries_timed": queries, "qmode": qmode_name(qm, qk)},
+        "frames_per_s": round(K / secs, 1),
+        "computed_queries_per_s": round(span["computed"] / secs, 1),
+        "gru_rows_per_s": round(span["gru_rows"] / secs, 1),
+        "score_hit_ratio": hit(span["score_hits"], span["queries"]),
+        "hist_hit_ratio": hit(span["hist_hits"], span["hists"]),
+        "wall_ms": round(wall * 1e3, 3),
+        "roofline": roofline,
+        "stages": stages,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(args, wl, qm, qk, sc, run, frames):
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import Oracle
+    cfg, m = wl.cfg, wl.cfg.model
+    o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
+               cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
+    t = time.perf_counter()
+    nq = S = 0
+    for fr in wl.frames:
+        o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
+        nq += fr.n_query
+        S += 1
+        if time.perf_counter() - t >= args.cpu_seconds:
+            break
+    secs = time.perf_counter() - t
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    # the GPU on exactly the same frames (cold caches, frame 0 on)
+    sc.reset()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(0, S)
+    e1.record()
+    torch.cuda.synchronize()
+    gsec = e0.elapsed_time(e1) / 1e3
+    log("oracle: %d frames, %d queries in %.1fs" % (S, nq, secs))
+    return {"value": round(nq / secs, 1), "unit": "queries/s", "cores": int(threads), "kind": "oracle",
+            "sample": "frames 0..%d of the same workload from empty caches (%d queries, %.1f s)"
+                      % (S - 1, nq, secs),
+            "gpu_value_same_sample": round(nq / gsec, 1)}
+
+
+if __name__ == "__main__":
+    main()
