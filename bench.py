@@ -69,21 +69,37 @@ def qmode_name(qm, k):
     return {0: "exact", 1: "sign", 2: "sigdig%d" % k}[qm]
 
 
-def algorithmic_work(cfg, st, qm):
-    """Algorithmic FLOPs / bytes of each stage over a span with stats `st`."""
+def algorithmic_work(cfg, st, qm, frames):
+    """Algorithmic FLOPs / bytes of each stage over a span with stats `st`.
+
+    The GRU step is a contraction: FLOPs = 2 * 3H * (Kx + H) per row and
+    layer. With few rows per frame its weights dominate instead (every frame
+    must read all 3H x (Kx + H) weights once), so it is priced against
+    whichever roofline is slower for the measured row count.
+    """
     m = cfg.model
     wb = 2 if m.wdtype == 1 else 4
     LH, H, E = m.L * m.H, m.H, m.E
     cw_bytes = {0: LH * 4, 1: LH // 8, 2: LH * 2}[qm]
-    flop_row = sum(2 * 3 * H * ((E if l == 0 else H) + H) for l in range(m.L))
+    K = [(E if l == 0 else H) + H for l in range(m.L)]
+    flop_row = sum(2 * 3 * H * k for k in K)
+    w_bytes = sum(3 * H * k * wb for k in K)
+    row_bytes = sum(k * 4 + 2 * H * 4 for k in K)
+    gru_flops = st["gru_rows"] * flop_row
+    gru_bytes = frames * w_bytes + st["gru_rows"] * row_bytes
+    mfma_peak = PEAK["bf16_mfma_TFs"] if m.wdtype == 1 else PEAK["fp32_mfma_TFs"]
+    gru = ("mfma", gru_flops) if gru_flops / (mfma_peak * 1e12) >= gru_bytes / (PEAK["hbm_GBs"] * 1e9) \
+        else ("hbm", gru_bytes)
     orders = max(0, m.maxent_order - 1)
     computed = st["computed"] + st["query_dups"]
     per_q = H * wb + 4 + 4 * orders + 8 + 4          # row, bias, MaxEnt, ids, score
     return {
-        "gru_gemm": ("mfma", st["gru_rows"] * flop_row),
-        "score": ("hbm", computed * per_q + st["score_hits"] * 16 + st["hists"] * H * 4),
+        "gru_gemm": gru,
+        # scores (row gathers, h' reads, MaxEnt) + h' copy-out + history-cache inserts
+        "score_finish": ("hbm", computed * per_q + st["score_hits"] * 16 + st["hists"] * H * 4
+                         + 2 * st["hists"] * LH * 4 + st["hist_inserted"] * cw_bytes),
+        # history vectors in, codes out, hashes, cache-hit code comparisons
         "hist_key": ("hbm", st["hists"] * (LH * 4 + 12 + cw_bytes + 8) + st["hist_hits"] * cw_bytes),
-        "hist_finish": ("hbm", 2 * st["hists"] * LH * 4 + st["hist_inserted"] * cw_bytes),
     }
 
 
@@ -169,12 +185,12 @@ def main():
     if not args.no_replay:
         sc.reset()
         run(0, W)
-        sc.profile(R.STAGES[:8])
+        sc.profile(R.STAGES[:4])
         run(W, n_frames)
         torch.cuda.synchronize()
         prof = sc.profile_read()
         sc.profile(())
-        work = algorithmic_work(cfg, span, qm)
+        work = algorithmic_work(cfg, span, qm, K)
         for name, (ms, launches) in prof.items():
             entry = {"ms_total": round(ms, 4), "launches": launches, "us_per_launch": round(1e3 * ms / launches, 2)}
             if name in work:

@@ -78,8 +78,8 @@ typedef struct {
     int32_t maxent_order;  /* n-gram orders 2..maxent_order are summed (1..4; 1 = none) */
     int32_t qmode;         /* RNNLM_Q_* */
     int32_t qdigits;       /* significant digits for RNNLM_Q_SIGDIG, 1..3 */
-    int32_t max_hist;      /* largest n_hist of any frame */
-    int32_t max_query;     /* largest n_query of any frame */
+    int32_t max_hist;      /* largest n_hist of any frame, 1..2048 */
+    int32_t max_query;     /* largest n_query of any frame, 0..8192 */
     int32_t pad0;
     int64_t cap_hist;      /* history-cache entries (admission stops when full) */
     int64_t cap_query;     /* LM-query cache entries */
@@ -162,10 +162,9 @@ int rnnlm_debug_quantize(int32_t qmode, int32_t qdigits, const float *x, int64_t
                          void *codes, int32_t *err, void *stream);
 
 /* Benchmark hook: per-stage kernel timing with HIP events recorded on the
- * frame's stream. Stages (bit i of stage_mask): 0 history keys, 1 history
- * plan, 2 query keys, 3 query resolve, 4 query admission, 5 GRU GEMM (all
- * layers), 6 scoring, 7 history finish, 8 normaliser GEMM, 9 normaliser
- * combine. Only masked stages get events (each pair adds a little time
+ * frame's stream. Stages (bit i of stage_mask): 0 history keys, 1 frame
+ * plan (de-duplication, cache probes, admission), 2 GRU GEMM (all layers),
+ * 3 scoring and frame finish, 8 normaliser GEMM, 9 normaliser combine. Only masked stages get events (each pair adds a little time
  * between kernels). stage_mask = 0 turns timing off and releases the events.
  * The events are host-side HIP objects; no device memory is allocated. */
 enum { RNNLM_NSTAGES = 10 };

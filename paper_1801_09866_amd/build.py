@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librnnlm.so")
-SOURCES = ["api.hip", "keys.hip", "gru.hip", "score.hip", "lognorm.hip"]
+SOURCES = ["api.hip", "keys.hip", "plan.hip", "gru.hip", "score.hip", "lognorm.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -18,6 +18,7 @@ struct rnnlm_t {
     rnnlm_config cfg;
     rn::Dev dev;
     unsigned host_derr;   // sticky device error as last read by rnnlm_get_stats
+    int pending_parts = 0;   // scoring blocks of the last frame whose counts are not folded yet
     // optional per-stage timing (rnnlm_profile)
     uint32_t prof_mask = 0;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_pool;   // created events
@@ -131,8 +132,10 @@ int check_config(const rnnlm_config *c) {
     if (c->qmode < RNNLM_Q_EXACT || c->qmode > RNNLM_Q_SIGDIG) return fail(RNNLM_EINVAL, "bad qmode");
     if (c->qmode == RNNLM_Q_SIGDIG && (c->qdigits < 1 || c->qdigits > 3))
         return fail(RNNLM_EINVAL, "qdigits must be 1..3");
-    if (c->max_hist < 1 || c->max_hist > (1 << 22)) return fail(RNNLM_EINVAL, "max_hist out of range");
-    if (c->max_query < 0 || c->max_query > (1 << 24)) return fail(RNNLM_EINVAL, "max_query out of range");
+    if (c->max_hist < 1 || c->max_hist > rn::kPlanMaxHist)
+        return fail(RNNLM_EINVAL, "max_hist must be 1..%d", rn::kPlanMaxHist);
+    if (c->max_query < 0 || c->max_query > rn::kPlanMaxQuery)
+        return fail(RNNLM_EINVAL, "max_query must be 0..%d", rn::kPlanMaxQuery);
     if (c->cap_hist < 0 || c->cap_hist > (1LL << 28)) return fail(RNNLM_EINVAL, "cap_hist out of range");
     if (c->cap_query < 0 || c->cap_query > (1LL << 29)) return fail(RNNLM_EINVAL, "cap_query out of range");
     return RNNLM_OK;
@@ -152,15 +155,13 @@ struct Carver {
 };
 
 struct Extents {
-    uint32_t HI, SI, FT, QT;
+    uint32_t HI, SI;   // open-addressing table sizes (load <= 1/2)
 };
 
 Extents extents(const rnnlm_config &c) {
     Extents e;
     e.HI = pow2_at_least(2 * c.cap_hist);
     e.SI = pow2_at_least(2 * c.cap_query);
-    e.FT = pow2_at_least(2LL * c.max_hist);
-    e.QT = pow2_at_least(2LL * (c.max_query > 0 ? c.max_query : 1));
     return e;
 }
 
@@ -179,53 +180,38 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
         }
     }
     const size_t mh = c.max_hist, mq = c.max_query > 0 ? c.max_query : 1;
-    const size_t ch = c.cap_hist > 0 ? c.cap_hist : 1, cq = c.cap_query > 0 ? c.cap_query : 1;
-    d.hc_islot = cv.take<int>(x.HI);
-    d.hc_ihash = cv.take<unsigned long long>(x.HI);
+    const size_t ch = c.cap_hist > 0 ? c.cap_hist : 1;
+    d.hc_idx = cv.take<rn::HcIdx>(x.HI);
     d.hc_codes = cv.take<unsigned long long>(ch * CW);
-    d.hc_word = cv.take<int>(ch);
     d.hc_val = cv.take<float>(ch * LH);
-    d.sc_islot = cv.take<int>(x.SI);
-    d.sc_ihash = cv.take<unsigned long long>(x.SI);
-    d.sc_key = cv.take<int4>(cq);
-    d.sc_val = cv.take<float>(cq);
+    d.sc_tab = cv.take<rn::ScEnt>(x.SI);
+    d.sc_stage = cv.take<rn::ScEnt>(mq);
     d.ctr = cv.take<long long>(rn::C_N);
     d.derr = cv.take<unsigned>(1);
     d.f_codes = cv.take<unsigned long long>(mh * CW);
     d.f_hhash = cv.take<unsigned long long>(mh);
     d.f_words = cv.take<int>(mh * 3);
     d.f_hcslot = cv.take<int>(mh);
-    d.f_hrep = cv.take<int>(mh);
     d.f_hstat = cv.take<int>(mh);
     d.f_hslot = cv.take<int>(mh);
-    d.f_ftpos = cv.take<int>(mh);
     d.f_hptr = cv.take<unsigned long long>(mh);
     d.f_rows = cv.take<int>(mh);
     d.f_rowdst = cv.take<unsigned long long>(mh);
     d.f_hval = cv.take<float>(mh * LH);
-    d.ft_hash = cv.take<unsigned long long>(x.FT);
-    d.ft_min = cv.take<int>(x.FT);
     d.f_qkey = cv.take<int4>(mq);
-    d.f_qhist = cv.take<int>(mq);
-    d.f_qsc = cv.take<int>(mq);
-    d.f_qrep = cv.take<int>(mq);
-    d.f_qstat = cv.take<int>(mq);
+    d.f_qw1 = cv.take<int>(mq);
+    d.f_qrec = cv.take<rn::QRec>(mq);
     d.f_qcand = cv.take<int>(mq);
-    d.f_qadmit = cv.take<int>(mq);
-    d.f_qtpos = cv.take<int>(mq);
-    d.qt_hash = cv.take<unsigned long long>(x.QT);
-    d.qt_min = cv.take<int>(x.QT);
+    d.f_part = cv.take<int4>((mq + 3) / 4);
     d.ln_part = cv.take<float2>((size_t)256 * rn::lognorm_tiles(c.V));
     return (cv.off + 255) & ~(size_t)255;
 }
 
+// Empty caches (index slot / entry key = -1) and zero counters, with fill
+// kernels rather than memsets so the sequence can live in a captured graph.
 void reset_state(const rn::Dev &d, const Extents &x, hipStream_t s) {
-    rn::launch_fill_u32(d.hc_islot, 0xFFFFFFFFu, x.HI, s);
-    rn::launch_fill_u32(d.sc_islot, 0xFFFFFFFFu, x.SI, s);
-    rn::launch_fill_u32(d.ft_hash, 0u, 2LL * x.FT, s);
-    rn::launch_fill_u32(d.ft_min, 0x7FFFFFFFu, x.FT, s);
-    rn::launch_fill_u32(d.qt_hash, 0u, 2LL * x.QT, s);
-    rn::launch_fill_u32(d.qt_min, 0x7FFFFFFFu, x.QT, s);
+    rn::launch_fill_u32(d.hc_idx, 0xFFFFFFFFu, (long long)x.HI * sizeof(rn::HcIdx) / 4, s);
+    rn::launch_fill_u32(d.sc_tab, 0xFFFFFFFFu, (long long)x.SI * sizeof(rn::ScEnt) / 4, s);
     rn::launch_fill_u32(d.ctr, 0u, 2LL * rn::C_N, s);
     rn::launch_fill_u32(d.derr, 0u, 1, s);
 }
@@ -265,7 +251,7 @@ RNNLM_API int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void
     d.qmode = cfg->qmode; d.qdigits = cfg->qmode == RNNLM_Q_SIGDIG ? cfg->qdigits : 0;
     d.max_hist = cfg->max_hist; d.max_query = cfg->max_query; d.CW = code_words(*cfg);
     d.cap_hist = cfg->cap_hist; d.cap_query = cfg->cap_query; d.seed = cfg->seed;
-    d.hi_mask = x.HI - 1; d.si_mask = x.SI - 1; d.ft_mask = x.FT - 1; d.qt_mask = x.QT - 1;
+    d.hi_mask = x.HI - 1; d.si_mask = x.SI - 1;
     d.emb = w->emb; d.U_out = w->U_out; d.b_out = w->b_out; d.maxent = w->maxent;
     for (int l = 0; l < 2; ++l) {
         d.Wp[l] = packed[l];
@@ -308,18 +294,13 @@ RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const rn::Dev &d = ctx->dev;
     { StageTimer t(ctx, s, 0); rn::launch_hist_key(d, f, decades(), s); }
-    { StageTimer t(ctx, s, 1); rn::launch_hist_plan(d, f, s); }
-    if (f.n_query > 0) {
-        { StageTimer t(ctx, s, 2); rn::launch_query_key(d, f, s); }
-        { StageTimer t(ctx, s, 3); rn::launch_query_resolve(d, f, s); }
-        { StageTimer t(ctx, s, 4); rn::launch_query_admit(d, f, s); }
-    }
+    { StageTimer t(ctx, s, 1); rn::launch_frame_plan(d, f, ctx->pending_parts, s); }
     {
-        StageTimer t(ctx, s, 5);
+        StageTimer t(ctx, s, 2);
         for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, f, l, f.n_hist, s);
     }
-    if (f.n_query > 0) { StageTimer t(ctx, s, 6); rn::launch_score(d, f, s); }
-    { StageTimer t(ctx, s, 7); rn::launch_hist_finish(d, f, s); }
+    { StageTimer t(ctx, s, 3); rn::launch_score_finish(d, f, s); }
+    ctx->pending_parts = (f.n_query + 3) / 4;
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "rnnlm_score_frame launch");
     return RNNLM_OK;
@@ -331,6 +312,7 @@ RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "rnnlm_cache_reset launch");
     ctx->host_derr = 0;
+    ctx->pending_parts = 0;
     return RNNLM_OK;
 }
 
@@ -358,7 +340,10 @@ RNNLM_API int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *st, void *stream) {
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     long long c[rn::C_N];
     unsigned derr = 0;
-    hipError_t e = hipMemcpyAsync(c, ctx->dev.ctr, sizeof c, hipMemcpyDeviceToHost, s);
+    rn::launch_fold_stats(ctx->dev, ctx->pending_parts, s);   // counts the last frame's scoring blocks left
+    ctx->pending_parts = 0;
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess) e = hipMemcpyAsync(c, ctx->dev.ctr, sizeof c, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(&derr, ctx->dev.derr, sizeof derr, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "rnnlm_get_stats");

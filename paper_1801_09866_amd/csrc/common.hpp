@@ -13,13 +13,19 @@ typedef unsigned long long u64;   // the integer type HIP 64-bit atomics take
 constexpr u64 kPhi = 0x9E3779B97F4A7C15ull;   // SplitMix64 increment (2^64 / golden ratio)
 constexpr int kMaxLH = 2048;                       // largest L*H (codes staged in LDS)
 constexpr int kMaxCW = kMaxLH / 2;                 // largest code-word count (EXACT: 2 per word)
+constexpr int kPlanMaxHist = 2048;                 // frame planner limits (LDS tables)
+constexpr int kPlanMaxQuery = 8192;
 
 // Counter slots in the device counter array (int64 each).
 enum Ctr {
     C_HC_SIZE = 0, C_SC_SIZE, C_FRAMES, C_QUERIES, C_SCORE_HITS, C_QUERY_DUPS, C_COMPUTED,
     C_HISTS, C_HIST_HITS, C_HIST_DUPS, C_GRU_ROWS, C_HIST_INS, C_HIST_REJ, C_SCORE_INS,
-    C_SCORE_REJ, C_FRAME_M, C_N
+    C_SCORE_REJ, C_FRAME_M, C_STAGED, C_NEAR_CAP, C_DONE, C_N
 };
+
+// QRec flag bits above the 2-bit base status (COMPUTED or Q_DUP)
+constexpr int QF_CAND = 16;    // first of its key with a cached history key: may be admitted
+constexpr int QF_PROBE = 32;   // the history key was cached before the frame: probe the LM cache
 
 // Frame arguments as the kernels see them.
 struct FrameArgs {
@@ -37,13 +43,38 @@ struct DecadeTab {
     uint32_t lo[21];
 };
 
+// History-cache index record (open addressing, 16 B): slot -1 = empty.
+struct HcIdx {
+    u64 hash;
+    int slot;   // dense entry (codes + h') of this key
+    int word;   // GRU input word of the key
+};
+
+// LM-query cache entry (open addressing, 32 B, key stored in place): hs -1 = empty.
+struct ScEnt {
+    int hs;     // history-cache slot of the query's history key
+    int w2, w3; // MaxEnt context words of the key (-1 where the orders do not use them)
+    int t;      // target word
+    float val;  // stored fp32 score
+    int pad[3];
+};
+
+// What the scorer needs per query, written by the frame planner (32 B).
+struct QRec {
+    u64 hptr;   // address of the history's top-layer h' (or the stored score bits on a hit)
+    int t;      // target word
+    int flags;  // bits 0-1 base status (COMPUTED / Q_DUP), QF_CAND, QF_PROBE; bits 6.. staging slot
+    int hs;     // history-cache slot after the frame (-1: not cached)
+    int w1, w2, w3;   // w-1 and the key's context words (-1 where unused)
+};
+
 // Everything a kernel needs to know about one context (passed by value).
 struct Dev {
     // configuration
     int V, E, H, L, LH, wdtype, me_log2, me_order, qmode, qdigits, max_hist, max_query, CW;
     long long cap_hist, cap_query;
     unsigned long long seed;
-    uint32_t hi_mask, si_mask, ft_mask, qt_mask;
+    uint32_t hi_mask, si_mask;
     // weights (borrowed) and packed GRU weights [3H][Kx + H] per layer
     const void *emb;
     const void *Wp[2];
@@ -51,38 +82,35 @@ struct Dev {
     const void *U_out;
     const float *b_out;
     const float *maxent;
-    // history cache: open-addressing index (slot id, key hash) + dense entries
-    int *hc_islot;
-    u64 *hc_ihash;
-    u64 *hc_codes;   // [cap_hist][CW]
-    int *hc_word;                   // [cap_hist]
-    float *hc_val;                  // [cap_hist][LH]
-    // LM-query (score) cache: index + dense entries (hist slot, w-2, w-3, target) -> score
-    int *sc_islot;
-    u64 *sc_ihash;
-    int4 *sc_key;
-    float *sc_val;
+    // history cache: index + dense entries
+    HcIdx *hc_idx;
+    u64 *hc_codes;    // [cap_hist][CW]
+    float *hc_val;    // [cap_hist][LH]
+    // LM-query cache, and the scores admitted this frame (entered into the
+    // table by the next frame's keys kernel, so probes always see the cache as
+    // it was before the frame)
+    ScEnt *sc_tab;
+    ScEnt *sc_stage;  // [max_query]
     // statistics and sticky error bits
     long long *ctr;
     unsigned *derr;
     // per-frame history scratch
-    u64 *f_codes;    // [max_hist][CW]
+    u64 *f_codes;     // [max_hist][CW]
     u64 *f_hhash;
-    int *f_words;                   // [max_hist][3], ids clamped into [0, V)
-    int *f_hcslot;                  // cache slot found before the frame, or -1
-    int *f_hrep, *f_hstat, *f_hslot, *f_ftpos;
-    u64 *f_hptr;     // device address of each history's h' (all layers)
-    int *f_rows;                    // GRU work list: history index of row r
-    u64 *f_rowdst;   // where row r writes its h'
-    float *f_hval;                  // [max_hist][LH] h' of rows the cache did not admit
-    u64 *ft_hash;    // per-frame history table (cleared after the frame)
-    int *ft_min;
+    int *f_words;     // [max_hist][3], ids clamped into [0, V)
+    int *f_hcslot;    // cache slot found before the frame, or -1
+    int *f_hstat, *f_hslot;
+    u64 *f_hptr;      // device address of each history's h' (all layers)
+    int *f_rows;      // GRU work list: history index of row r
+    u64 *f_rowdst;    // where row r writes its h'
+    float *f_hval;    // [max_hist][LH] h' of rows the cache did not admit
     // per-frame query scratch
-    int4 *f_qkey;                   // (history representative, w-2, w-3, target)
-    int *f_qhist, *f_qsc, *f_qrep, *f_qstat, *f_qcand, *f_qadmit, *f_qtpos;
-    u64 *qt_hash;
-    int *qt_min;
-    // normaliser partials [max_hist][n_tiles] of (max, sum exp)
+    int4 *f_qkey;     // (history index, w-2, w-3, target) for exact key checks
+    int *f_qw1;       // w-1 of each query's history
+    QRec *f_qrec;
+    int *f_qcand;     // admission candidates (used when the cache is nearly full)
+    int4 *f_part;     // per scoring block: (computed, duplicates, hits, admitted), folded later
+    // normaliser partials [256][n_tiles] of (max, sum exp)
     float2 *ln_part;
 };
 
@@ -104,6 +132,13 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // butterfly sum over the 64 lanes; every lane ends with the same value
+// Index of the calling wave in its block, as a scalar. The compiler cannot
+// prove threadIdx.x >> 6 uniform across a wave; branches on a value it takes
+// for divergent become exec-masked regions, and a matrix instruction inside
+// such a region still writes its accumulator when no lane is active. Every
+// branch around an MFMA must therefore depend on scalars only.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -116,12 +151,57 @@ __device__ __forceinline__ u64 wave_sum_u64(u64 v) {
     return v;
 }
 
-// 64-bit hash of a query key (for table placement only)
-__device__ __forceinline__ u64 query_hash(int a, int b, int c, int d) {
-    u64 g = mix64((u64)(uint32_t)a + kPhi);
+// 64-bit hash of a query key (for table placement only); `a` identifies the
+// history key (its cache slot, or its 64-bit key hash within a frame)
+__device__ __forceinline__ u64 query_hash(u64 a, int b, int c, int d) {
+    u64 g = mix64(a + kPhi);
     g = mix64(g ^ (u64)(uint32_t)(b + 2));
     g = mix64(g ^ (u64)(uint32_t)(c + 2));
     return mix64(g ^ (u64)(uint32_t)(d + 1));
+}
+
+// Counts of the last frame's scoring blocks (per-block records, written
+// without atomics), added into a copy of the counters `c` held in LDS. Run by
+// one block; every thread must call it.
+__device__ __forceinline__ void fold_partials(const Dev &d, int n, long long *c, int *s_red) {
+    int a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+    for (int b = threadIdx.x; b < n; b += blockDim.x) {
+        const int4 p = d.f_part[b];
+        a0 += p.x; a1 += p.y; a2 += p.z; a3 += p.w;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        a0 += __shfl_xor(a0, o, 64);
+        a1 += __shfl_xor(a1, o, 64);
+        a2 += __shfl_xor(a2, o, 64);
+        a3 += __shfl_xor(a3, o, 64);
+    }
+    if (threadIdx.x < 4) s_red[threadIdx.x] = 0;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) {
+        atomicAdd(&s_red[0], a0);
+        atomicAdd(&s_red[1], a1);
+        atomicAdd(&s_red[2], a2);
+        atomicAdd(&s_red[3], a3);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        c[C_COMPUTED] += s_red[0];
+        c[C_QUERY_DUPS] += s_red[1];
+        c[C_SCORE_HITS] += s_red[2];
+        c[C_SCORE_INS] += s_red[3];
+        c[C_SC_SIZE] += s_red[3];
+    }
+    __syncthreads();
+}
+
+// 32-bit finaliser of MurmurHash3 (Appleby), for frame-local table placement
+__device__ __forceinline__ uint32_t fmix32(uint32_t h) {
+    h ^= h >> 16;
+    h *= 0x85EBCA6Bu;
+    h ^= h >> 13;
+    h *= 0xC2B2AE35u;
+    return h ^ (h >> 16);
 }
 
 // slot of the order-n MaxEnt n-gram (w-1 .. w-(n-1), target) in a 2^log2 table

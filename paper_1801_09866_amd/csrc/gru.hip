@@ -90,22 +90,315 @@ __device__ __forceinline__ void gru_epilogue(const Dev &d, const FrameArgs &f, i
     }
 }
 
+__device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
+    uint4 r;
+    r.x = (uint32_t)f32_to_bf16(a.x) | ((uint32_t)f32_to_bf16(a.y) << 16);
+    r.y = (uint32_t)f32_to_bf16(a.z) | ((uint32_t)f32_to_bf16(a.w) << 16);
+    r.z = (uint32_t)f32_to_bf16(b.x) | ((uint32_t)f32_to_bf16(b.y) << 16);
+    r.w = (uint32_t)f32_to_bf16(b.z) | ((uint32_t)f32_to_bf16(b.w) << 16);
+    return r;
+}
+
+// ------------------------ skinny path (few rows) --------------------------
+// In steady state most history keys are cached and a frame has only a few new
+// keys. Then the weights (not the FLOPs) are the cost: each block takes 4
+// hidden units (12 packed weight rows) for every row; its 8 waves split into
+// 4 units x 2 halves of K, with the rows' [x ; h] staged in LDS once per
+// block. Blocks are dealt to XCDs so that each XCD streams a contiguous 1/8
+// of the weights.
+constexpr int S_UNITS = 4;          // hidden units per block
+constexpr int S_MAXROWS = 16;       // rows handled by the skinny path at most
+constexpr int S_BATCH = 8;          // K chunks whose weights are fetched together
+constexpr int S_LDS_FLOATS = 24576; // 96 KB LDS buffer shared with the MFMA path
+constexpr int S_PART = 4 * 4 * S_MAXROWS;               // second-half partial sums
+constexpr int S_A_FLOATS = S_LDS_FLOATS - S_PART;       // staged rows
+
+__device__ __forceinline__ int skinny_rows(int K) {
+    const int r = S_A_FLOATS / K;
+    return r < S_MAXROWS ? r : S_MAXROWS;
+}
+
+template <bool BF16W>
+__device__ void gru_skinny(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int b) {
+    const int NB = d.H / S_UNITS;
+    const int g = (NB & 7) == 0 ? (b & 7) * (NB >> 3) + (b >> 3) : b;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H;
+    const int K = Kx + d.H;
+    float *sA = smem;
+    float *sP = smem + S_A_FLOATS;
+
+    // stage the M rows [x ; h] (bf16 weights: rows rounded to bf16, as the MFMA path does)
+    for (int m = 0; m < M; ++m) {
+        const RowSrc src = row_source(d, f, layer, m, M);
+        for (int k = tid * 4; k < K; k += G_THREADS * 4) {
+            float4 v;
+            if (k < Kx) {
+                if (src.x_bf16) {
+                    const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(src.x) + k);
+                    v = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                                    __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+                } else {
+                    v = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src.x) + k);
+                }
+            } else {
+                v = *reinterpret_cast<const float4 *>(src.h + (k - Kx));
+            }
+            if (BF16W) {
+                v.x = bf16_to_f32(f32_to_bf16(v.x));
+                v.y = bf16_to_f32(f32_to_bf16(v.y));
+                v.z = bf16_to_f32(f32_to_bf16(v.z));
+                v.w = bf16_to_f32(f32_to_bf16(v.w));
+            }
+            *reinterpret_cast<float4 *>(sA + m * K + k) = v;
+        }
+    }
+    __syncthreads();
+
+    const int u = w & 3, half = w >> 2;
+    const int j = g * S_UNITS + u;
+    const size_t rr = (size_t)j * K, rz = (size_t)(d.H + j) * K, rn_ = (size_t)(2 * d.H + j) * K;
+    float ar[S_MAXROWS], az[S_MAXROWS], anx[S_MAXROWS], anh[S_MAXROWS];
+#pragma unroll
+    for (int m = 0; m < S_MAXROWS; ++m) ar[m] = az[m] = anx[m] = anh[m] = 0.0f;
+    auto wload = [&](size_t off) -> float {
+        if (BF16W) return bf16_to_f32(reinterpret_cast<const uint16_t *>(d.Wp[layer])[off]);
+        return reinterpret_cast<const float *>(d.Wp[layer])[off];
+    };
+    // 64-wide chunks of K; the first half of the chunks to waves 0-3, the rest
+    // to 4-7. Weights are fetched S_BATCH chunks at a time, so each batch costs
+    // one memory round trip rather than one per chunk.
+    const int nc = K / 64, c0 = half ? nc / 2 : 0, c1 = half ? nc : nc / 2;
+    for (int cb = c0; cb < c1; cb += S_BATCH) {
+        float wr[S_BATCH], wz[S_BATCH], wn[S_BATCH];
+#pragma unroll
+        for (int u2 = 0; u2 < S_BATCH; ++u2) {
+            const int k = (cb + u2) * 64 + lane;
+            const bool ok = cb + u2 < c1;
+            wr[u2] = ok ? wload(rr + k) : 0.0f;
+            wz[u2] = ok ? wload(rz + k) : 0.0f;
+            wn[u2] = ok ? wload(rn_ + k) : 0.0f;
+        }
+#pragma unroll
+        for (int u2 = 0; u2 < S_BATCH; ++u2) {
+            const int c = cb + u2;
+            if (c >= c1) break;   // wave-uniform
+            const int k = c * 64 + lane;
+            if (c * 64 < Kx) {    // input part (chunk-uniform): candidate's input accumulator
+#pragma unroll
+                for (int m = 0; m < S_MAXROWS; ++m) {
+                    if (m < M) {
+                        const float a = sA[m * K + k];
+                        ar[m] = fmaf(a, wr[u2], ar[m]);
+                        az[m] = fmaf(a, wz[u2], az[m]);
+                        anx[m] = fmaf(a, wn[u2], anx[m]);
+                    }
+                }
+            } else {              // recurrent part: candidate's recurrent accumulator
+#pragma unroll
+                for (int m = 0; m < S_MAXROWS; ++m) {
+                    if (m < M) {
+                        const float a = sA[m * K + k];
+                        ar[m] = fmaf(a, wr[u2], ar[m]);
+                        az[m] = fmaf(a, wz[u2], az[m]);
+                        anh[m] = fmaf(a, wn[u2], anh[m]);
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < S_MAXROWS; ++m) {
+        if (m < M) {
+            ar[m] = wave_sum(ar[m]);
+            az[m] = wave_sum(az[m]);
+            anx[m] = wave_sum(anx[m]);
+            anh[m] = wave_sum(anh[m]);
+            if (half && lane == 0) {
+                float *p = sP + (u * S_MAXROWS + m) * 4;
+                p[0] = ar[m];
+                p[1] = az[m];
+                p[2] = anx[m];
+                p[3] = anh[m];
+            }
+        }
+    }
+    __syncthreads();
+    if (half) return;   // the caller's next tile starts with a barrier
+    const float *bb = d.b_ih[layer];
+    const float br = bb[j], bz = bb[d.H + j], bn = bb[2 * d.H + j];
+#pragma unroll
+    for (int m = 0; m < S_MAXROWS; ++m) {
+        if (m < M && lane == 0) {
+            const float *p = sP + (u * S_MAXROWS + m) * 4;
+            const int i = d.f_rows[m];
+            const float hprev = f.hist_vec[(size_t)i * d.LH + (size_t)layer * d.H + j];
+            const float r = sigmoidf_(ar[m] + p[0] + br);
+            const float z = sigmoidf_(az[m] + p[1] + bz);
+            const float n = tanhf(anx[m] + p[2] + bn + r * (anh[m] + p[3]));
+            float *dst = reinterpret_cast<float *>(d.f_rowdst[m]) + (size_t)layer * d.H + j;
+            *dst = (1.0f - z) * n + z * hprev;
+        }
+    }
+}
+
+// ------------------------ medium path (16 < rows <= 256) -------------------
+// Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
+// accumulating the four gate tiles (reset, update, candidate input part,
+// candidate recurrent part) of its K range with MFMAs fed straight from
+// global memory (16 B per lane per step, one step prefetched), then the
+// partial tiles are summed through LDS and wave 0 applies the gates.
+constexpr int MD_MAXROWS = 256;
+
+template <bool BF16W>
+__device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, float *smem) {
+    const int NJ = d.H / 16;
+    const int ntiles = ((M + 15) / 16) * NJ;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H, K = Kx + d.H;
+    constexpr int KS = BF16W ? 32 : 16;            // k per MFMA step
+    const int nsteps = K / KS;
+    const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;
+    const int row = lane & 15, kq = (KS / 4) * (lane >> 4);
+    for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        int mt, jt;
+        if ((NJ & 7) == 0) {   // every XCD keeps its own unit tiles (and weights)
+            const int xcd = tile & 7, idx = tile >> 3, per = NJ >> 3;
+            mt = idx / per;
+            jt = xcd + 8 * (idx % per);
+        } else {
+            mt = tile / NJ;
+            jt = tile % NJ;
+        }
+        const int m0 = mt * 16, j0 = jt * 16;
+        const RowSrc src = row_source(d, f, layer, m0 + row, M);
+        const size_t wr = (size_t)(j0 + row) * K, wz = (size_t)(d.H + j0 + row) * K,
+                     wn = (size_t)(2 * d.H + j0 + row) * K;
+        f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
+        if (!BF16W) {
+            const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
+            auto loadA = [&](int k) -> float4 {
+                if (!src.valid) return make_float4(0.f, 0.f, 0.f, 0.f);
+                if (k < Kx) return *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src.x) + k);
+                return *reinterpret_cast<const float4 *>(src.h + (k - Kx));
+            };
+            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), br = a, bz = a, bn = a;
+            if (s0 < s1) {
+                const int k = s0 * KS + kq;
+                a = loadA(k);
+                br = *reinterpret_cast<const float4 *>(Wp + wr + k);
+                bz = *reinterpret_cast<const float4 *>(Wp + wz + k);
+                bn = *reinterpret_cast<const float4 *>(Wp + wn + k);
+            }
+            for (int st = s0; st < s1; ++st) {
+                float4 a2 = a, br2 = br, bz2 = bz, bn2 = bn;
+                if (st + 1 < s1) {
+                    const int k = (st + 1) * KS + kq;
+                    a2 = loadA(k);
+                    br2 = *reinterpret_cast<const float4 *>(Wp + wr + k);
+                    bz2 = *reinterpret_cast<const float4 *>(Wp + wz + k);
+                    bn2 = *reinterpret_cast<const float4 *>(Wp + wn + k);
+                }
+                const float av[4] = {a.x, a.y, a.z, a.w};
+                const float rv[4] = {br.x, br.y, br.z, br.w};
+                const float zv[4] = {bz.x, bz.y, bz.z, bz.w};
+                const float nv[4] = {bn.x, bn.y, bn.z, bn.w};
+                if (st * KS < Kx) {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
+                        az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
+                        anx = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anx, 0, 0, 0);
+                    }
+                } else {
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
+                        az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
+                        anh = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anh, 0, 0, 0);
+                    }
+                }
+                a = a2; br = br2; bz = bz2; bn = bn2;
+            }
+        } else {
+            const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wp[layer]);
+            auto loadA = [&](int k) -> uint4 {
+                if (!src.valid) return make_uint4(0, 0, 0, 0);
+                if (k < Kx) {
+                    if (src.x_bf16) return *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(src.x) + k);
+                    const float *p = reinterpret_cast<const float *>(src.x) + k;
+                    return pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
+                }
+                const float *p = src.h + (k - Kx);
+                return pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
+            };
+            uint4 a = make_uint4(0, 0, 0, 0), br = a, bz = a, bn = a;
+            if (s0 < s1) {
+                const int k = s0 * KS + kq;
+                a = loadA(k);
+                br = *reinterpret_cast<const uint4 *>(Wp + wr + k);
+                bz = *reinterpret_cast<const uint4 *>(Wp + wz + k);
+                bn = *reinterpret_cast<const uint4 *>(Wp + wn + k);
+            }
+            for (int st = s0; st < s1; ++st) {
+                uint4 a2 = a, br2 = br, bz2 = bz, bn2 = bn;
+                if (st + 1 < s1) {
+                    const int k = (st + 1) * KS + kq;
+                    a2 = loadA(k);
+                    br2 = *reinterpret_cast<const uint4 *>(Wp + wr + k);
+                    bz2 = *reinterpret_cast<const uint4 *>(Wp + wz + k);
+                    bn2 = *reinterpret_cast<const uint4 *>(Wp + wn + k);
+                }
+                const bf8_t av = __builtin_bit_cast(bf8_t, a);
+                ar = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, br), ar, 0, 0, 0);
+                az = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bz), az, 0, 0, 0);
+                if (st * KS < Kx) anx = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bn), anx, 0, 0, 0);
+                else anh = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bn), anh, 0, 0, 0);
+                a = a2; br = br2; bz = bz2; bn = bn2;
+            }
+        }
+        // sum the waves' partial tiles, then the gates (wave 0)
+        float *red = smem + (size_t)(w * 64 + lane) * 16;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            red[e] = ar[e];
+            red[4 + e] = az[e];
+            red[8 + e] = anx[e];
+            red[12 + e] = anh[e];
+        }
+        __syncthreads();
+        if (w == 0) {
+            for (int v = 1; v < 8; ++v) {
+                const float *o = smem + (size_t)(v * 64 + lane) * 16;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    ar[e] += o[e];
+                    az[e] += o[4 + e];
+                    anx[e] += o[8 + e];
+                    anh[e] += o[12 + e];
+                }
+            }
+            gru_epilogue(d, f, layer, M, m0, j0, 0, 0, ar, az, anx, anh);
+        }
+        __syncthreads();   // the partial tiles are reused by the next tile
+    }
+}
+
 // ------------------------------- fp32 -------------------------------------
 constexpr int F_BK = 32;
 constexpr int F_LDA = F_BK + 4;   // padded LDS row (floats)
 
-__global__ __launch_bounds__(G_THREADS) void k_gru_f32(Dev d, FrameArgs f, int layer) {
-    const int M = (int)d.ctr[C_FRAME_M];
+__device__ void gru_mfma_f32(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int tile) {
     const int NJ = d.H / G_BJ;
     int mt, jt;
-    gru_tile_of(blockIdx.x, NJ, mt, jt);
+    gru_tile_of(tile, NJ, mt, jt);
     const int m0 = mt * G_BM, j0 = jt * G_BJ;
     if (m0 >= M) return;
 
-    __shared__ float As[2][G_BM][F_LDA];
-    __shared__ float Bs[2][3 * G_BJ][F_LDA];
+    auto As = reinterpret_cast<float (*)[G_BM][F_LDA]>(smem);
+    auto Bs = reinterpret_cast<float (*)[3 * G_BJ][F_LDA]>(smem + 2 * G_BM * F_LDA);
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
@@ -183,27 +476,19 @@ __global__ __launch_bounds__(G_THREADS) void k_gru_f32(Dev d, FrameArgs f, int l
 constexpr int H_BK = 64;
 constexpr int H_LDA = H_BK + 8;   // padded LDS row (bf16 elements)
 
-__device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
-    uint4 r;
-    r.x = (uint32_t)f32_to_bf16(a.x) | ((uint32_t)f32_to_bf16(a.y) << 16);
-    r.y = (uint32_t)f32_to_bf16(a.z) | ((uint32_t)f32_to_bf16(a.w) << 16);
-    r.z = (uint32_t)f32_to_bf16(b.x) | ((uint32_t)f32_to_bf16(b.y) << 16);
-    r.w = (uint32_t)f32_to_bf16(b.z) | ((uint32_t)f32_to_bf16(b.w) << 16);
-    return r;
-}
 
-__global__ __launch_bounds__(G_THREADS) void k_gru_bf16(Dev d, FrameArgs f, int layer) {
-    const int M = (int)d.ctr[C_FRAME_M];
+__device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int tile) {
     const int NJ = d.H / G_BJ;
     int mt, jt;
-    gru_tile_of(blockIdx.x, NJ, mt, jt);
+    gru_tile_of(tile, NJ, mt, jt);
     const int m0 = mt * G_BM, j0 = jt * G_BJ;
     if (m0 >= M) return;
 
-    __shared__ uint16_t As[2][G_BM][H_LDA];
-    __shared__ uint16_t Bs[2][3 * G_BJ][H_LDA];
+    uint16_t *sm16 = reinterpret_cast<uint16_t *>(smem);
+    auto As = reinterpret_cast<uint16_t (*)[G_BM][H_LDA]>(sm16);
+    auto Bs = reinterpret_cast<uint16_t (*)[3 * G_BJ][H_LDA]>(sm16 + 2 * G_BM * H_LDA);
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wp[layer]);
@@ -270,6 +555,32 @@ __global__ __launch_bounds__(G_THREADS) void k_gru_bf16(Dev d, FrameArgs f, int 
     gru_epilogue(d, f, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
 }
 
+// One launch per layer; the device-side row count picks the path.
+static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= S_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
+static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= S_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
+
+template <bool BF16W>
+__global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, FrameArgs f, int layer) {
+    __shared__ __align__(16) float smem[S_LDS_FLOATS];
+    const int M = (int)d.ctr[C_FRAME_M];
+    if (M <= 0) return;
+    const int K = (layer == 0 ? d.E : d.H) + d.H;
+    if (M <= skinny_rows(K)) {        // few rows: stream the weights through the VALU
+        for (int t = blockIdx.x; t < d.H / S_UNITS; t += gridDim.x) {
+            __syncthreads();
+            gru_skinny<BF16W>(d, f, layer, M, smem, t);
+        }
+    } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
+        gru_medium<BF16W>(d, f, layer, M, smem);
+    } else {                          // 64 x 32 MFMA tiles through LDS
+        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / G_BJ);
+        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+            if (BF16W) gru_mfma_bf16(d, f, layer, M, smem, t);
+            else gru_mfma_f32(d, f, layer, M, smem, t);
+        }
+    }
+}
+
 // --------------------------- weight packing -------------------------------
 __global__ void k_pack_layer(const void *W_ih, const void *W_hh, void *dst, int rows, int Kx, int H,
                              int elem) {
@@ -300,14 +611,12 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
 
 void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s) {
     if (max_rows <= 0) return;
-    const int NJ = d.H / G_BJ;
-    const int NM = (max_rows + G_BM - 1) / G_BM;
-    int blocks = NM * NJ;
-    if ((NJ & 7) == 0) blocks = ((blocks + 7) / 8) * 8;   // whole rounds over the XCDs
+    // one block per CU (the LDS buffer allows no more); blocks loop over tiles
+    const int blocks = 256;
     if (d.wdtype == RNNLM_BF16)
-        k_gru_bf16<<<blocks, G_THREADS, 0, s>>>(d, f, layer);
+        k_gru<true><<<blocks, G_THREADS, 0, s>>>(d, f, layer);
     else
-        k_gru_f32<<<blocks, G_THREADS, 0, s>>>(d, f, layer);
+        k_gru<false><<<blocks, G_THREADS, 0, s>>>(d, f, layer);
 }
 
 }  // namespace rn

@@ -6,12 +6,10 @@
 namespace rn {
 
 void launch_fill_u32(void *p, uint32_t v, long long n, hipStream_t s);
+void launch_fold_stats(const Dev &d, int npart, hipStream_t s);
 void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, hipStream_t s);
-void launch_hist_plan(const Dev &d, const FrameArgs &f, hipStream_t s);
-void launch_query_key(const Dev &d, const FrameArgs &f, hipStream_t s);
-void launch_query_resolve(const Dev &d, const FrameArgs &f, hipStream_t s);
-void launch_query_admit(const Dev &d, const FrameArgs &f, hipStream_t s);
-void launch_hist_finish(const Dev &d, const FrameArgs &f, hipStream_t s);
+void launch_frame_plan(const Dev &d, const FrameArgs &f, int npart, hipStream_t s);
+void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s);
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s);
 
@@ -22,7 +20,6 @@ void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows,
 void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_hh, void *dst,
                        hipStream_t s);
 
-void launch_score(const Dev &d, const FrameArgs &f, hipStream_t s);
 
 int lognorm_tiles(int V);
 void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s);

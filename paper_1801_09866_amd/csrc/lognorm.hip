@@ -19,7 +19,7 @@ int lognorm_tiles(int V) { return (V + LN_BN - 1) / LN_BN; }
 __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int n) {
     __shared__ float As[2][LN_BM][LN_LD];
     __shared__ float Bs[2][LN_BN][LN_LD];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int tile = blockIdx.x, v0 = tile * LN_BN;
     const int H = d.H, V = d.V;
     const float *U = reinterpret_cast<const float *>(d.U_out);

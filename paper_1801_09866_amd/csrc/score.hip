@@ -1,26 +1,54 @@
-// Query scoring (Sec. 2.2 NCE, Sec. 2.3 MaxEnt): one wave per query.
-//   score = U_out[t] . h'_top + b_out[t] + sum_{n=2..N} maxent[slot_n]
-// The output row is read once, coalesced across the wave (16 B per lane per
-// step), and reduced with a fixed butterfly, so every query with the same key
-// produces the same bits. Stored scores are returned for cache hits, and new
-// admitted keys are entered into the LM-query cache.
+// Scoring and frame finish, one launch (blocks of 4 waves):
+//   query waves (Sec. 2.2 NCE, Sec. 2.3 MaxEnt), one wave per query:
+//     probe the LM-query cache (Sec. 2.4) if the history key was cached; on a
+//     hit return the stored score, else
+//       score = U_out[t] . h'_top + b_out[t] + sum_{n=2..N} maxent[slot_n]
+//     The output row is read once, coalesced across the wave (16 B per lane
+//     per step), and reduced with a fixed butterfly, so equal keys produce
+//     equal bits. Admitted new keys are staged; the next frame's keys kernel
+//     enters them into the table, so every probe of this frame sees the cache
+//     as it was before the frame.
+//   history waves, one per history record: admitted new history keys go into
+//     the history-cache index (their h' is already in place), and h' is
+//     copied to the caller's output.
+// Admission order only matters when the frame's candidates could overflow
+// the LM-query cache; then the last block to finish admits them in ascending
+// query index.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace rn {
 
+// staging slot e receives a new LM-query cache entry (hs = -1: slot unused)
+__device__ __forceinline__ void stage_score(const Dev &d, long long e, int hs, int w2, int w3, int t, float s) {
+    ScEnt en;
+    en.hs = hs;
+    en.w2 = w2;
+    en.w3 = w3;
+    en.t = t;
+    en.val = s;
+    en.pad[0] = en.pad[1] = en.pad[2] = 0;
+    d.sc_stage[e] = en;
+}
+
 template <bool BF16>
-__global__ __launch_bounds__(256) void k_score(Dev d, FrameArgs f) {
-    const int q = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-    if (q >= f.n_query) return;
-    const int st = d.f_qstat[q];
-    const int4 key = d.f_qkey[q];
-    const int i = d.f_qhist[q], t = key.w;
-    float s;
-    if (st == RNNLM_Q_SCORE_HIT) {
-        s = d.sc_val[d.f_qsc[q]];
-    } else {
-        const float *h = reinterpret_cast<const float *>(d.f_hptr[i]) + (size_t)(d.L - 1) * d.H;
+__device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, int q, int lane, bool near_cap,
+                                            int *s_cnt) {
+    const QRec rec = d.f_qrec[q];
+    const int t = rec.t;
+    bool hit = false;
+    float s = 0.0f;
+    if (rec.flags & QF_PROBE) {
+        unsigned pos = (unsigned)(query_hash((u64)rec.hs, rec.w2, rec.w3, t) & d.si_mask);
+        for (unsigned k = 0; k <= d.si_mask; ++k) {
+            const ScEnt e = d.sc_tab[pos];
+            if (e.hs < 0) break;
+            if (e.hs == rec.hs && e.w2 == rec.w2 && e.w3 == rec.w3 && e.t == t) { hit = true; s = e.val; break; }
+            pos = (pos + 1) & d.si_mask;
+        }
+    }
+    if (!hit) {
+        const float *h = reinterpret_cast<const float *>(rec.hptr);
         float acc = 0.0f;
         if (!BF16) {
             const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
@@ -48,40 +76,146 @@ __global__ __launch_bounds__(256) void k_score(Dev d, FrameArgs f) {
                 acc = fmaf(__uint_as_float(a.w & 0xFFFF0000u), b1.w, acc);
             }
         }
-        s = wave_sum(acc);
-        s += d.b_out[t];
-        const int w1 = d.f_words[i * 3], w2 = d.f_words[i * 3 + 1], w3 = d.f_words[i * 3 + 2];
-        for (int o = 2; o <= d.me_order; ++o) s += d.maxent[maxent_slot(o, w1, w2, w3, t, d.me_log2)];
+        // MaxEnt weights and bias are loaded while the row is in flight
+        float me = d.b_out[t];
+        for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, rec.w1, rec.w2, rec.w3, t, d.me_log2)];
+        s = wave_sum(acc) + me;
     }
     if (lane == 0) {
+        const int st = hit ? RNNLM_Q_SCORE_HIT : (rec.flags & 3);
         f.scores[q] = s;
-        const int id = d.f_qadmit[q];
-        if (id >= 0) {
-            const int hs = d.f_hslot[i];
-            d.sc_key[id] = make_int4(hs, key.y, key.z, t);
-            d.sc_val[id] = s;
-            const u64 sh = query_hash(hs, key.y, key.z, t);
-            unsigned pos = (unsigned)(sh & d.si_mask);
-            for (unsigned n = 0; n <= d.si_mask; ++n) {
-                if (atomicCAS(&d.sc_islot[pos], -1, id) == -1) {
-                    d.sc_ihash[pos] = sh;
-                    break;
-                }
-                pos = (pos + 1) & d.si_mask;
-            }
+        if (f.q_status) f.q_status[q] = (uint8_t)st;
+        atomicAdd(&s_cnt[st], 1);
+        const bool cand = !hit && (rec.flags & QF_CAND);
+        if (near_cap) {
+            d.f_qcand[q] = cand ? 1 : 0;
+        } else if (rec.flags & QF_CAND) {   // own staging slot: entry, or unused on a hit
+            stage_score(d, rec.flags >> 6, cand ? rec.hs : -1, rec.w2, rec.w3, t, s);
+            if (cand) atomicAdd(&s_cnt[3], 1);
         }
-        const int tp = d.f_qtpos[q];
-        d.qt_hash[tp] = 0ull;
-        d.qt_min[tp] = 0x7FFFFFFF;
     }
 }
 
-void launch_score(const Dev &d, const FrameArgs &f, hipStream_t s) {
-    const int blocks = (f.n_query + 3) / 4;
+__device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f, int i, int lane) {
+    if (d.f_hstat[i] == RNNLM_H_REP) {
+        const int slot = d.f_hslot[i];
+        if (slot >= 0) {
+            const u64 *src = d.f_codes + (size_t)i * d.CW;
+            u64 *dst = d.hc_codes + (size_t)slot * d.CW;
+            for (int w = lane; w < d.CW; w += 64) dst[w] = src[w];
+            if (lane == 0) {
+                const u64 h = d.f_hhash[i];
+                unsigned pos = (unsigned)(h & d.hi_mask);
+                for (unsigned n = 0; n <= d.hi_mask; ++n) {
+                    HcIdx *r = d.hc_idx + pos;
+                    if (atomicCAS(&r->slot, -1, slot) == -1) {
+                        r->hash = h;
+                        r->word = d.f_words[i * 3];
+                        break;
+                    }
+                    pos = (pos + 1) & d.hi_mask;
+                }
+            }
+        }
+    }
+    if (f.hnew) {
+        const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
+        float4 *dst = reinterpret_cast<float4 *>(f.hnew + (size_t)i * d.LH);
+        for (int e = lane; e < d.LH / 4; e += 64) dst[e] = src[e];
+    }
+}
+
+// exclusive scan over a 256-thread block
+__device__ int scan256(int v, int *s_tmp, int *total) {
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) s_tmp[wv] = x;
+    __syncthreads();
+    int base = 0;
+    for (int k = 0; k < wv; ++k) base += s_tmp[k];
+    *total = s_tmp[0] + s_tmp[1] + s_tmp[2] + s_tmp[3];
+    __syncthreads();
+    return base + x - v;
+}
+
+// ordered admission for a frame whose candidates could overflow the cache:
+// ascending query index while the cache has room (run by the last block)
+__device__ void admit_in_order(const Dev &d, const FrameArgs &f, int *s_tmp) {
+    const long long size0 = d.ctr[C_SC_SIZE];
+    int carry = 0, ins = 0, rej = 0;
+    __shared__ int s_ins, s_rej;
+    if (threadIdx.x == 0) s_ins = s_rej = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < f.n_query; c0 += 256) {
+        const int q = c0 + threadIdx.x;
+        const int cand = q < f.n_query ? d.f_qcand[q] : 0;
+        int total;
+        const int rank = scan256(cand, s_tmp, &total) + carry;
+        if (cand) {
+            if (size0 + rank < d.cap_query) {
+                const QRec rec = d.f_qrec[q];
+                stage_score(d, rank, rec.hs, rec.w2, rec.w3, rec.t, f.scores[q]);
+                ++ins;
+            } else {
+                ++rej;
+            }
+        }
+        carry += total;
+    }
+    if (ins) atomicAdd(&s_ins, ins);
+    if (rej) atomicAdd(&s_rej, rej);
+    __syncthreads();
+    if (threadIdx.x == 0) {   // the only writer of these counters in this frame
+        d.ctr[C_SCORE_INS] += s_ins;
+        d.ctr[C_SCORE_REJ] += s_rej;
+        d.ctr[C_SC_SIZE] += s_ins;
+        d.ctr[C_STAGED] = s_ins;   // admitted entries occupy staging slots 0 .. s_ins-1
+    }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_score_finish(Dev d, FrameArgs f, int qblocks) {
+    __shared__ int s_cnt[4];
+    __shared__ int s_tmp[8];
+    __shared__ int s_last;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const bool near_cap = d.ctr[C_NEAR_CAP] != 0;
+    if (tid < 4) s_cnt[tid] = 0;
+    __syncthreads();
+    if ((int)blockIdx.x < qblocks) {
+        const int q = blockIdx.x * 4 + w;
+        if (q < f.n_query) score_query<BF16>(d, f, q, lane, near_cap, s_cnt);
+    } else {
+        const int i = (blockIdx.x - qblocks) * 4 + w;
+        if (i < f.n_hist) finish_history(d, f, i, lane);
+    }
+    __syncthreads();
+    if (tid == 0 && (int)blockIdx.x < qblocks)   // folded into the counters by the next planner
+        d.f_part[blockIdx.x] = make_int4(s_cnt[RNNLM_Q_COMPUTED], s_cnt[RNNLM_Q_DUP], s_cnt[RNNLM_Q_SCORE_HIT],
+                                         s_cnt[3]);
+    if (!near_cap) return;   // grid-uniform
+    // last block to finish admits this frame's candidates in order
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) s_last = atomicAdd((unsigned long long *)&d.ctr[C_DONE], 1ull) == (unsigned long long)(gridDim.x - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    admit_in_order(d, f, s_tmp);
+    if (tid == 0) d.ctr[C_DONE] = 0;
+}
+
+void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s) {
+    const int qb = (f.n_query + 3) / 4, hb = (f.n_hist + 3) / 4;
     if (d.wdtype == RNNLM_BF16)
-        k_score<true><<<blocks, 256, 0, s>>>(d, f);
+        k_score_finish<true><<<qb + hb, 256, 0, s>>>(d, f, qb);
     else
-        k_score<false><<<blocks, 256, 0, s>>>(d, f);
+        k_score_finish<false><<<qb + hb, 256, 0, s>>>(d, f, qb);
 }
 
 }  // namespace rn

@@ -63,8 +63,8 @@ EXPORTS = ("rnnlm_workspace_size", "rnnlm_create", "rnnlm_score_frame", "rnnlm_c
            "rnnlm_log_normalizer", "rnnlm_get_stats", "rnnlm_debug_quantize", "rnnlm_profile",
            "rnnlm_profile_read", "rnnlm_destroy", "rnnlm_last_error")
 NSTAGES = 10
-STAGES = ("hist_key", "hist_plan", "query_key", "query_resolve", "query_admit", "gru_gemm",
-          "score", "hist_finish", "lognorm_gemm", "lognorm_combine")
+STAGES = ("hist_key", "frame_plan", "gru_gemm", "score_finish", "unused4", "unused5",
+          "unused6", "unused7", "lognorm_gemm", "lognorm_combine")
 
 _lib = None
 
