@@ -100,6 +100,10 @@ def algorithmic_work(cfg, st, qm, frames):
                          + 2 * st["hists"] * LH * 4 + st["hist_inserted"] * cw_bytes),
         # history vectors in, codes out, hashes, cache-hit code comparisons
         "hist_key": ("hbm", st["hists"] * (LH * 4 + 12 + cw_bytes + 8) + st["hist_hits"] * cw_bytes),
+        # the plan: per history hash + cache slot in, status/rep/slot/h' address out; per query
+        # key + w-1 in, 32 B work record + rep out; per GRU row its source and destination
+        "frame_plan": ("hbm", st["hists"] * (8 + 4 + 1 + 4 + 4 + 8 + 1) + st["queries"] * (16 + 4 + 32 + 4)
+                       + st["gru_rows"] * (4 + 8)),
     }
 
 
@@ -205,7 +209,7 @@ def main():
                     entry.update(bound="hbm", achieved=round(ach, 1), peak=PEAK["hbm_GBs"], unit="GB/s",
                                  frac=round(ach / PEAK["hbm_GBs"], 4), algorithmic=amount)
             stages[name] = entry
-        dom = max((n for n in stages if "bound" in stages[n]), key=lambda n: stages[n]["ms_total"])
+        dom = max(stages, key=lambda n: stages[n]["ms_total"])
         e = stages[dom]
         roofline = {"kernel": dom, "bound": e["bound"], "achieved": e["achieved"], "peak": e["peak"],
                     "unit": e["unit"], "frac": e["frac"], "traffic": None,

@@ -161,12 +161,15 @@ int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *stats, void *stream);
 int rnnlm_debug_quantize(int32_t qmode, int32_t qdigits, const float *x, int64_t n,
                          void *codes, int32_t *err, void *stream);
 
-/* Benchmark hook: per-stage kernel timing with HIP events recorded on the
- * frame's stream. Stages (bit i of stage_mask): 0 history keys, 1 frame
- * plan (de-duplication, cache probes, admission), 2 GRU GEMM (all layers),
- * 3 scoring and frame finish, 8 normaliser GEMM, 9 normaliser combine. Only masked stages get events (each pair adds a little time
- * between kernels). stage_mask = 0 turns timing off and releases the events.
- * The events are host-side HIP objects; no device memory is allocated. */
+/* Benchmark hook: per-stage kernel timing. Stages (bit i of stage_mask):
+ * 0 history keys, 1 frame plan (de-duplication, cache probes, admission),
+ * 2 GRU GEMM (all layers), 3 scoring and frame finish, 8 normaliser GEMM,
+ * 9 normaliser combine. A timed stage's kernels are launched with a HIP
+ * start/stop event pair that their dispatch packets stamp (hipExtLaunchKernel),
+ * so a stage's time runs from the start of its first kernel to the end of its
+ * last and excludes the gaps between stages. stage_mask = 0 turns timing off
+ * and releases the events. The events are host-side HIP objects; no device
+ * memory is allocated. */
 enum { RNNLM_NSTAGES = 10 };
 int rnnlm_profile(rnnlm_t *ctx, uint32_t stage_mask);
 

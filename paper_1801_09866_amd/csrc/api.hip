@@ -19,6 +19,7 @@ struct rnnlm_t {
     rn::Dev dev;
     unsigned host_derr;   // sticky device error as last read by rnnlm_get_stats
     int pending_parts = 0;   // scoring blocks of the last frame whose counts are not folded yet
+    int staged_max = 0;      // bound on the scores the last frame staged for the LM-query cache
     // optional per-stage timing (rnnlm_profile)
     uint32_t prof_mask = 0;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_pool;   // created events
@@ -28,13 +29,11 @@ struct rnnlm_t {
 
 namespace {
 
-// Brackets one stage's launches with an event pair when that stage is timed.
+// Hands out a start/stop event pair for one stage's launches when that stage
+// is timed; the kernels' own dispatch packets take the timestamps.
 struct StageTimer {
-    rnnlm_t *ctx;
-    hipStream_t s;
-    int stage;
-    hipEvent_t end = nullptr;
-    StageTimer(rnnlm_t *c, hipStream_t st, int stg) : ctx(c), s(st), stage(stg) {
+    rn::Stamp ts;
+    StageTimer(rnnlm_t *ctx, int stage) {
         if (!(ctx->prof_mask & (1u << stage))) return;
         if (ctx->prof_used == ctx->prof_pool.size()) {
             hipEvent_t a, b;
@@ -44,11 +43,15 @@ struct StageTimer {
         }
         auto &pr = ctx->prof_pool[ctx->prof_used++];
         ctx->prof_stage.push_back(stage);
-        (void)hipEventRecord(pr.first, s);
-        end = pr.second;
+        ts.start = pr.first;
+        ts.stop = pr.second;
     }
-    ~StageTimer() {
-        if (end) (void)hipEventRecord(end, s);
+    // stamps for kernel k of a stage of n kernels
+    rn::Stamp part(int k, int n) const {
+        rn::Stamp p;
+        if (k == 0) p.start = ts.start;
+        if (k == n - 1) p.stop = ts.stop;
+        return p;
     }
 };
 
@@ -196,6 +199,7 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.f_hslot = cv.take<int>(mh);
     d.f_hptr = cv.take<unsigned long long>(mh);
     d.f_rows = cv.take<int>(mh);
+    d.f_roww = cv.take<int>(mh);
     d.f_rowdst = cv.take<unsigned long long>(mh);
     d.f_hval = cv.take<float>(mh * LH);
     d.f_qkey = cv.take<int4>(mq);
@@ -293,14 +297,16 @@ RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm
     f.q_rep = out->q_rep; f.h_rep = out->h_rep; f.h_hash = reinterpret_cast<rn::u64 *>(out->h_hash);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     const rn::Dev &d = ctx->dev;
-    { StageTimer t(ctx, s, 0); rn::launch_hist_key(d, f, decades(), s); }
-    { StageTimer t(ctx, s, 1); rn::launch_frame_plan(d, f, ctx->pending_parts, s); }
+    rn::launch_hist_key(d, f, decades(), ctx->staged_max, ctx->pending_parts, s, StageTimer(ctx, 0).ts);
+    ctx->pending_parts = 0;
+    rn::launch_frame_plan(d, f, s, StageTimer(ctx, 1).ts);
     {
-        StageTimer t(ctx, s, 2);
-        for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, f, l, f.n_hist, s);
+        const StageTimer t(ctx, 2);
+        for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, f, l, f.n_hist, s, t.part(l, c.L));
     }
-    { StageTimer t(ctx, s, 3); rn::launch_score_finish(d, f, s); }
+    rn::launch_score_finish(d, f, s, StageTimer(ctx, 3).ts);
     ctx->pending_parts = (f.n_query + 3) / 4;
+    ctx->staged_max = f.n_query;
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "rnnlm_score_frame launch");
     return RNNLM_OK;
@@ -313,6 +319,7 @@ RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
     if (e != hipSuccess) return hip_fail(e, "rnnlm_cache_reset launch");
     ctx->host_derr = 0;
     ctx->pending_parts = 0;
+    ctx->staged_max = 0;
     return RNNLM_OK;
 }
 
@@ -327,8 +334,8 @@ RNNLM_API int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, 
     for (int r0 = 0; r0 < n; r0 += 256) {
         const int nr = n - r0 < 256 ? n - r0 : 256;
         const float *hb = h_top + (size_t)r0 * ctx->cfg.H;
-        { StageTimer t(ctx, s, 8); rn::launch_lognorm_gemm(ctx->dev, hb, nr, s); }
-        { StageTimer t(ctx, s, 9); rn::launch_lognorm_combine(ctx->dev, nr, logz + r0, s); }
+        rn::launch_lognorm_gemm(ctx->dev, hb, nr, s, StageTimer(ctx, 8).ts);
+        rn::launch_lognorm_combine(ctx->dev, nr, logz + r0, s, StageTimer(ctx, 9).ts);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "rnnlm_log_normalizer launch");

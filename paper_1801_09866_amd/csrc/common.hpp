@@ -102,6 +102,7 @@ struct Dev {
     int *f_hstat, *f_hslot;
     u64 *f_hptr;      // device address of each history's h' (all layers)
     int *f_rows;      // GRU work list: history index of row r
+    int *f_roww;      // GRU input word (w-1) of row r
     u64 *f_rowdst;    // where row r writes its h'
     float *f_hval;    // [max_hist][LH] h' of rows the cache did not admit
     // per-frame query scratch

@@ -10,6 +10,8 @@
 //   r = sigmoid(a_r), z = sigmoid(a_z), n = tanh(a_nx + b_n + r * a_nh),
 //   h' = (1 - z) * n + z * h.
 // The epilogue is fused: no gate pre-activation ever reaches HBM.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -55,7 +57,7 @@ __device__ __forceinline__ RowSrc row_source(const Dev &d, const FrameArgs &f, i
     const int i = d.f_rows[m];
     r.h = f.hist_vec + (size_t)i * d.LH + (size_t)layer * d.H;
     if (layer == 0) {
-        const int w = d.f_words[i * 3];
+        const int w = d.f_roww[m];   // loaded beside f_rows, not after it
         if (d.wdtype == RNNLM_BF16) {
             r.x = reinterpret_cast<const uint16_t *>(d.emb) + (size_t)w * d.E;
             r.x_bf16 = true;
@@ -75,17 +77,28 @@ __device__ __forceinline__ void gru_epilogue(const Dev &d, const FrameArgs &f, i
     const int j = j0 + ub * 16 + (lane & 15);
     const float *b = d.b_ih[layer];
     const float br = b[j], bz = b[d.H + j], bn = b[2 * d.H + j];
+    // every load first (the stores could alias them as far as the compiler
+    // knows, which would serialise one round trip per row)
+    int mrow[4], hist[4];
+    float *dst[4];
+    float hprev[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        const int m = m0 + rb * 16 + 4 * (lane >> 4) + e;
-        if (m < M) {
-            const int i = d.f_rows[m];
-            const float hprev = f.hist_vec[(size_t)i * d.LH + (size_t)layer * d.H + j];
+        mrow[e] = m0 + rb * 16 + 4 * (lane >> 4) + e;
+        const bool ok = mrow[e] < M;
+        hist[e] = ok ? d.f_rows[mrow[e]] : 0;
+        dst[e] = ok ? reinterpret_cast<float *>(d.f_rowdst[mrow[e]]) : nullptr;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        hprev[e] = mrow[e] < M ? f.hist_vec[(size_t)hist[e] * d.LH + (size_t)layer * d.H + j] : 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        if (mrow[e] < M) {
             const float r = sigmoidf_(ar[e] + br);
             const float z = sigmoidf_(az[e] + bz);
             const float n = tanhf(anx[e] + bn + r * anh[e]);
-            float *dst = reinterpret_cast<float *>(d.f_rowdst[m]) + (size_t)layer * d.H + j;
-            *dst = (1.0f - z) * n + z * hprev;
+            dst[e][(size_t)layer * d.H + j] = (1.0f - z) * n + z * hprev[e];
         }
     }
 }
@@ -108,7 +121,7 @@ __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
 // of the weights.
 constexpr int S_UNITS = 4;          // hidden units per block
 constexpr int S_MAXROWS = 16;       // rows handled by the skinny path at most
-constexpr int S_BATCH = 8;          // K chunks whose weights are fetched together
+constexpr int S_CHUNKS = 16;        // 64-wide K chunks whose weights a wave fetches at once
 constexpr int S_LDS_FLOATS = 24576; // 96 KB LDS buffer shared with the MFMA path
 constexpr int S_PART = 4 * 4 * S_MAXROWS;               // second-half partial sums
 constexpr int S_A_FLOATS = S_LDS_FLOATS - S_PART;       // staged rows
@@ -128,29 +141,55 @@ __device__ void gru_skinny(const Dev &d, const FrameArgs &f, int layer, int M, f
     float *sA = smem;
     float *sP = smem + S_A_FLOATS;
 
-    // stage the M rows [x ; h] (bf16 weights: rows rounded to bf16, as the MFMA path does)
-    for (int m = 0; m < M; ++m) {
-        const RowSrc src = row_source(d, f, layer, m, M);
-        for (int k = tid * 4; k < K; k += G_THREADS * 4) {
-            float4 v;
-            if (k < Kx) {
-                if (src.x_bf16) {
-                    const uint2 u = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(src.x) + k);
-                    v = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
-                                    __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+    // the M rows' sources, resolved once, in parallel
+    __shared__ const void *s_x[S_MAXROWS];
+    __shared__ const float *s_h[S_MAXROWS];
+    __shared__ float *s_dst[S_MAXROWS];
+    if (tid < M) {
+        const RowSrc src = row_source(d, f, layer, tid, M);
+        s_x[tid] = src.x;
+        s_h[tid] = src.h;
+        s_dst[tid] = reinterpret_cast<float *>(d.f_rowdst[tid]) + (size_t)layer * d.H;
+    }
+    __syncthreads();
+    // stage the rows [x ; h] (bf16 weights: rows rounded to bf16, as the MFMA
+    // path does); SB float4 per thread are in flight at once
+    const bool xbf = layer == 0 && BF16W;
+    const int K4 = K / 4, n4 = M * K4;
+    constexpr int SB = 8;
+    for (int e0 = tid; e0 < n4; e0 += G_THREADS * SB) {
+        float4 v[SB];
+#pragma unroll
+        for (int q = 0; q < SB; ++q) {
+            const int e = e0 + q * G_THREADS;
+            if (e < n4) {
+                const int m = e / K4, k = (e - m * K4) * 4;
+                if (k < Kx) {
+                    if (xbf) {
+                        const uint2 u2 = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(s_x[m]) + k);
+                        v[q] = make_float4(__uint_as_float(u2.x << 16), __uint_as_float(u2.x & 0xFFFF0000u),
+                                           __uint_as_float(u2.y << 16), __uint_as_float(u2.y & 0xFFFF0000u));
+                    } else {
+                        v[q] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(s_x[m]) + k);
+                    }
                 } else {
-                    v = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src.x) + k);
+                    v[q] = *reinterpret_cast<const float4 *>(s_h[m] + (k - Kx));
                 }
-            } else {
-                v = *reinterpret_cast<const float4 *>(src.h + (k - Kx));
             }
-            if (BF16W) {
-                v.x = bf16_to_f32(f32_to_bf16(v.x));
-                v.y = bf16_to_f32(f32_to_bf16(v.y));
-                v.z = bf16_to_f32(f32_to_bf16(v.z));
-                v.w = bf16_to_f32(f32_to_bf16(v.w));
+        }
+#pragma unroll
+        for (int q = 0; q < SB; ++q) {
+            const int e = e0 + q * G_THREADS;
+            if (e < n4) {
+                float4 x = v[q];
+                if (BF16W) {
+                    x.x = bf16_to_f32(f32_to_bf16(x.x));
+                    x.y = bf16_to_f32(f32_to_bf16(x.y));
+                    x.z = bf16_to_f32(f32_to_bf16(x.z));
+                    x.w = bf16_to_f32(f32_to_bf16(x.w));
+                }
+                *reinterpret_cast<float4 *>(sA + e * 4) = x;   // row m at m * K
             }
-            *reinterpret_cast<float4 *>(sA + m * K + k) = v;
         }
     }
     __syncthreads();
@@ -166,100 +205,122 @@ __device__ void gru_skinny(const Dev &d, const FrameArgs &f, int layer, int M, f
         return reinterpret_cast<const float *>(d.Wp[layer])[off];
     };
     // 64-wide chunks of K; the first half of the chunks to waves 0-3, the rest
-    // to 4-7. Weights are fetched S_BATCH chunks at a time, so each batch costs
-    // one memory round trip rather than one per chunk.
-    const int nc = K / 64, c0 = half ? nc / 2 : 0, c1 = half ? nc : nc / 2;
-    for (int cb = c0; cb < c1; cb += S_BATCH) {
-        float wr[S_BATCH], wz[S_BATCH], wn[S_BATCH];
+    // to 4-7. All of a wave's weights are fetched at once (one memory round
+    // trip); the candidate gate's weight is split per chunk into its input and
+    // recurrent parts, so the row loop below has no branch. Rows go in groups
+    // of 4 and chunks in batches of 4: each (group, batch) issues its 16 LDS
+    // reads together.
+    const int nc = K / 64, h0 = half ? nc / 2 : 0, c1 = half ? nc : nc / 2;
+    for (int c0 = h0; c0 < c1; c0 += S_CHUNKS) {   // S_CHUNKS chunks per pass
+        float wr[S_CHUNKS], wz[S_CHUNKS], wnx[S_CHUNKS], wnh[S_CHUNKS];
 #pragma unroll
-        for (int u2 = 0; u2 < S_BATCH; ++u2) {
-            const int k = (cb + u2) * 64 + lane;
-            const bool ok = cb + u2 < c1;
+        for (int u2 = 0; u2 < S_CHUNKS; ++u2) {
+            const int c = c0 + u2;
+            const int k = c * 64 + lane;
+            const bool ok = c < c1;
             wr[u2] = ok ? wload(rr + k) : 0.0f;
             wz[u2] = ok ? wload(rz + k) : 0.0f;
-            wn[u2] = ok ? wload(rn_ + k) : 0.0f;
+            const float wn = ok ? wload(rn_ + k) : 0.0f;
+            const bool xpart = c * 64 < Kx;   // chunk-uniform
+            wnx[u2] = xpart ? wn : 0.0f;
+            wnh[u2] = xpart ? 0.0f : wn;
         }
 #pragma unroll
-        for (int u2 = 0; u2 < S_BATCH; ++u2) {
-            const int c = cb + u2;
-            if (c >= c1) break;   // wave-uniform
-            const int k = c * 64 + lane;
-            if (c * 64 < Kx) {    // input part (chunk-uniform): candidate's input accumulator
+        for (int g = 0; g < S_MAXROWS / 4; ++g) {
+            if (4 * g >= M) break;   // block-uniform
 #pragma unroll
-                for (int m = 0; m < S_MAXROWS; ++m) {
-                    if (m < M) {
-                        const float a = sA[m * K + k];
-                        ar[m] = fmaf(a, wr[u2], ar[m]);
-                        az[m] = fmaf(a, wz[u2], az[m]);
-                        anx[m] = fmaf(a, wn[u2], anx[m]);
-                    }
+            for (int cb = 0; cb < S_CHUNKS; cb += 4) {
+                if (c0 + cb >= c1) break;   // wave-uniform
+                float a[4][4];
+#pragma unroll
+                for (int u2 = 0; u2 < 4; ++u2) {
+                    const int k = min(c0 + cb + u2, c1 - 1) * 64 + lane;   // padded chunks: weight 0
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) a[u2][r] = sA[min(4 * g + r, M - 1) * K + k];
                 }
-            } else {              // recurrent part: candidate's recurrent accumulator
 #pragma unroll
-                for (int m = 0; m < S_MAXROWS; ++m) {
-                    if (m < M) {
-                        const float a = sA[m * K + k];
-                        ar[m] = fmaf(a, wr[u2], ar[m]);
-                        az[m] = fmaf(a, wz[u2], az[m]);
-                        anh[m] = fmaf(a, wn[u2], anh[m]);
+                for (int u2 = 0; u2 < 4; ++u2) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int m = 4 * g + r;
+                        ar[m] = fmaf(a[u2][r], wr[cb + u2], ar[m]);
+                        az[m] = fmaf(a[u2][r], wz[cb + u2], az[m]);
+                        anx[m] = fmaf(a[u2][r], wnx[cb + u2], anx[m]);
+                        anh[m] = fmaf(a[u2][r], wnh[cb + u2], anh[m]);
                     }
                 }
             }
         }
     }
+    // full sums in every lane; lane m then owns row m
+    float vr = 0.0f, vz = 0.0f, vnx = 0.0f, vnh = 0.0f;
 #pragma unroll
     for (int m = 0; m < S_MAXROWS; ++m) {
         if (m < M) {
-            ar[m] = wave_sum(ar[m]);
-            az[m] = wave_sum(az[m]);
-            anx[m] = wave_sum(anx[m]);
-            anh[m] = wave_sum(anh[m]);
-            if (half && lane == 0) {
-                float *p = sP + (u * S_MAXROWS + m) * 4;
-                p[0] = ar[m];
-                p[1] = az[m];
-                p[2] = anx[m];
-                p[3] = anh[m];
+            const float sr = wave_sum(ar[m]), sz = wave_sum(az[m]), snx = wave_sum(anx[m]), snh = wave_sum(anh[m]);
+            if (lane == m) {
+                vr = sr;
+                vz = sz;
+                vnx = snx;
+                vnh = snh;
             }
         }
     }
+    float4 *sP4 = reinterpret_cast<float4 *>(sP) + u * S_MAXROWS;
+    if (half && lane < M) sP4[lane] = make_float4(vr, vz, vnx, vnh);
     __syncthreads();
-    if (half) return;   // the caller's next tile starts with a barrier
+    if (half || lane >= M) return;   // the caller's next tile starts with a barrier
     const float *bb = d.b_ih[layer];
     const float br = bb[j], bz = bb[d.H + j], bn = bb[2 * d.H + j];
-#pragma unroll
-    for (int m = 0; m < S_MAXROWS; ++m) {
-        if (m < M && lane == 0) {
-            const float *p = sP + (u * S_MAXROWS + m) * 4;
-            const int i = d.f_rows[m];
-            const float hprev = f.hist_vec[(size_t)i * d.LH + (size_t)layer * d.H + j];
-            const float r = sigmoidf_(ar[m] + p[0] + br);
-            const float z = sigmoidf_(az[m] + p[1] + bz);
-            const float n = tanhf(anx[m] + p[2] + bn + r * (anh[m] + p[3]));
-            float *dst = reinterpret_cast<float *>(d.f_rowdst[m]) + (size_t)layer * d.H + j;
-            *dst = (1.0f - z) * n + z * hprev;
-        }
-    }
+    const float hprev = s_h[lane][j];
+    const float4 p = sP4[lane];
+    const float r = sigmoidf_(vr + p.x + br);
+    const float z = sigmoidf_(vz + p.y + bz);
+    const float n = tanhf(vnx + p.z + bn + r * (vnh + p.w));
+    s_dst[lane][j] = (1.0f - z) * n + z * hprev;
 }
 
 // ------------------------ medium path (16 < rows <= 256) -------------------
 // Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
 // accumulating the four gate tiles (reset, update, candidate input part,
 // candidate recurrent part) of its K range with MFMAs fed straight from
-// global memory (16 B per lane per step, one step prefetched), then the
-// partial tiles are summed through LDS and wave 0 applies the gates.
+// global memory (16 B per lane per operand and step), MD_CH steps in flight
+// at once, double-buffered; then the partial tiles are summed through LDS and
+// wave 0 applies the gates.
 constexpr int MD_MAXROWS = 256;
+constexpr int MD_CH = 2;
+
+template <bool BF16W>
+struct MdOps {
+    using T = typename std::conditional<BF16W, uint4, float4>::type;
+    T a[MD_CH], r[MD_CH], z[MD_CH], n[MD_CH];
+};
+
+// one K step of one gate tile: fp32 takes 4 k per lane (four 16x16x4 MFMAs
+// over the float4's components), bf16 takes 8 (one 16x16x32 MFMA)
+__device__ __forceinline__ f4_t md_mfma(float4 a, float4 b, f4_t c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+}
+__device__ __forceinline__ f4_t md_mfma(uint4 a, uint4 b, f4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8_t, a), __builtin_bit_cast(bf8_t, b), c, 0, 0, 0);
+}
 
 template <bool BF16W>
 __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, float *smem) {
+    using T = typename MdOps<BF16W>::T;
+    using E = typename std::conditional<BF16W, uint16_t, float>::type;
     const int NJ = d.H / 16;
     const int ntiles = ((M + 15) / 16) * NJ;
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H, K = Kx + d.H;
-    constexpr int KS = BF16W ? 32 : 16;            // k per MFMA step
+    constexpr int KS = BF16W ? 32 : 16;            // k per step
     const int nsteps = K / KS;
-    const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;
+    const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;   // scalars
     const int row = lane & 15, kq = (KS / 4) * (lane >> 4);
+    const E *Wp = reinterpret_cast<const E *>(d.Wp[layer]);
     for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         int mt, jt;
         if ((NJ & 7) == 0) {   // every XCD keeps its own unit tiles (and weights)
@@ -272,90 +333,52 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
         }
         const int m0 = mt * 16, j0 = jt * 16;
         const RowSrc src = row_source(d, f, layer, m0 + row, M);
-        const size_t wr = (size_t)(j0 + row) * K, wz = (size_t)(d.H + j0 + row) * K,
-                     wn = (size_t)(2 * d.H + j0 + row) * K;
+        const E *pr = Wp + (size_t)(j0 + row) * K + kq, *pz = Wp + (size_t)(d.H + j0 + row) * K + kq,
+                *pn = Wp + (size_t)(2 * d.H + j0 + row) * K + kq;
+        auto loadA = [&](int k) -> T {
+            if (!src.valid) return T{0, 0, 0, 0};
+            if (!BF16W) {
+                const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
+                return __builtin_bit_cast(T, *reinterpret_cast<const float4 *>(p));
+            }
+            if (k < Kx && src.x_bf16)
+                return __builtin_bit_cast(T, *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(src.x) + k));
+            const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
+            return __builtin_bit_cast(T, pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4)));
+        };
+        auto load = [&](MdOps<BF16W> &o, int sc) {
+#pragma unroll
+            for (int c = 0; c < MD_CH; ++c) {
+                const int st = sc + c;
+                if (st < s1) {
+                    const int k = st * KS;
+                    o.a[c] = loadA(k + kq);
+                    o.r[c] = *reinterpret_cast<const T *>(pr + k);
+                    o.z[c] = *reinterpret_cast<const T *>(pz + k);
+                    o.n[c] = *reinterpret_cast<const T *>(pn + k);
+                }
+            }
+        };
         f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-        if (!BF16W) {
-            const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
-            auto loadA = [&](int k) -> float4 {
-                if (!src.valid) return make_float4(0.f, 0.f, 0.f, 0.f);
-                if (k < Kx) return *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src.x) + k);
-                return *reinterpret_cast<const float4 *>(src.h + (k - Kx));
-            };
-            float4 a = make_float4(0.f, 0.f, 0.f, 0.f), br = a, bz = a, bn = a;
-            if (s0 < s1) {
-                const int k = s0 * KS + kq;
-                a = loadA(k);
-                br = *reinterpret_cast<const float4 *>(Wp + wr + k);
-                bz = *reinterpret_cast<const float4 *>(Wp + wz + k);
-                bn = *reinterpret_cast<const float4 *>(Wp + wn + k);
-            }
-            for (int st = s0; st < s1; ++st) {
-                float4 a2 = a, br2 = br, bz2 = bz, bn2 = bn;
-                if (st + 1 < s1) {
-                    const int k = (st + 1) * KS + kq;
-                    a2 = loadA(k);
-                    br2 = *reinterpret_cast<const float4 *>(Wp + wr + k);
-                    bz2 = *reinterpret_cast<const float4 *>(Wp + wz + k);
-                    bn2 = *reinterpret_cast<const float4 *>(Wp + wn + k);
-                }
-                const float av[4] = {a.x, a.y, a.z, a.w};
-                const float rv[4] = {br.x, br.y, br.z, br.w};
-                const float zv[4] = {bz.x, bz.y, bz.z, bz.w};
-                const float nv[4] = {bn.x, bn.y, bn.z, bn.w};
-                if (st * KS < Kx) {
+        auto compute = [&](const MdOps<BF16W> &o, int sc) {
 #pragma unroll
-                    for (int c = 0; c < 4; ++c) {
-                        ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
-                        az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
-                        anx = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anx, 0, 0, 0);
-                    }
-                } else {
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) {
-                        ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
-                        az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
-                        anh = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anh, 0, 0, 0);
-                    }
+            for (int c = 0; c < MD_CH; ++c) {
+                const int st = sc + c;
+                if (st < s1) {
+                    ar = md_mfma(o.a[c], o.r[c], ar);
+                    az = md_mfma(o.a[c], o.z[c], az);
+                    if (st * KS < Kx) anx = md_mfma(o.a[c], o.n[c], anx);
+                    else anh = md_mfma(o.a[c], o.n[c], anh);
                 }
-                a = a2; br = br2; bz = bz2; bn = bn2;
             }
-        } else {
-            const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wp[layer]);
-            auto loadA = [&](int k) -> uint4 {
-                if (!src.valid) return make_uint4(0, 0, 0, 0);
-                if (k < Kx) {
-                    if (src.x_bf16) return *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(src.x) + k);
-                    const float *p = reinterpret_cast<const float *>(src.x) + k;
-                    return pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
-                }
-                const float *p = src.h + (k - Kx);
-                return pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
-            };
-            uint4 a = make_uint4(0, 0, 0, 0), br = a, bz = a, bn = a;
-            if (s0 < s1) {
-                const int k = s0 * KS + kq;
-                a = loadA(k);
-                br = *reinterpret_cast<const uint4 *>(Wp + wr + k);
-                bz = *reinterpret_cast<const uint4 *>(Wp + wz + k);
-                bn = *reinterpret_cast<const uint4 *>(Wp + wn + k);
-            }
-            for (int st = s0; st < s1; ++st) {
-                uint4 a2 = a, br2 = br, bz2 = bz, bn2 = bn;
-                if (st + 1 < s1) {
-                    const int k = (st + 1) * KS + kq;
-                    a2 = loadA(k);
-                    br2 = *reinterpret_cast<const uint4 *>(Wp + wr + k);
-                    bz2 = *reinterpret_cast<const uint4 *>(Wp + wz + k);
-                    bn2 = *reinterpret_cast<const uint4 *>(Wp + wn + k);
-                }
-                const bf8_t av = __builtin_bit_cast(bf8_t, a);
-                ar = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, br), ar, 0, 0, 0);
-                az = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bz), az, 0, 0, 0);
-                if (st * KS < Kx) anx = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bn), anx, 0, 0, 0);
-                else anh = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf8_t, bn), anh, 0, 0, 0);
-                a = a2; br = br2; bz = bz2; bn = bn2;
-            }
+        };
+        MdOps<BF16W> b0, b1;
+        load(b0, s0);
+        for (int sc = s0; sc < s1; sc += 2 * MD_CH) {
+            load(b1, sc + MD_CH);
+            compute(b0, sc);
+            load(b0, sc + 2 * MD_CH);
+            compute(b1, sc + MD_CH);
         }
         // sum the waves' partial tiles, then the gates (wave 0)
         float *red = smem + (size_t)(w * 64 + lane) * 16;
@@ -609,14 +632,14 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
                                        d.wdtype == RNNLM_BF16 ? 2 : 4);
 }
 
-void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s) {
+void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s, Stamp ts) {
     if (max_rows <= 0) return;
     // one block per CU (the LDS buffer allows no more); blocks loop over tiles
     const int blocks = 256;
     if (d.wdtype == RNNLM_BF16)
-        k_gru<true><<<blocks, G_THREADS, 0, s>>>(d, f, layer);
+        launch_k(k_gru<true>, blocks, G_THREADS, s, ts, d, f, layer);
     else
-        k_gru<false><<<blocks, G_THREADS, 0, s>>>(d, f, layer);
+        launch_k(k_gru<false>, blocks, G_THREADS, s, ts, d, f, layer);
 }
 
 }  // namespace rn

@@ -1,28 +1,45 @@
 // Kernel launchers shared between the HIP translation units and the C ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 
 namespace rn {
 
+// Optional timestamps of a stage: the dispatch packet of its first kernel
+// stamps `start` when that kernel begins, the last kernel's stamps `stop` when
+// it ends (hipExtLaunchKernel), so the elapsed time is kernel execution only.
+struct Stamp {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
+template <typename... KArgs, typename... Args>
+inline void launch_k(void (*k)(KArgs...), unsigned grid, unsigned block, hipStream_t s, Stamp ts, Args... args) {
+    hipExtLaunchKernelGGL(k, dim3(grid), dim3(block), 0, s, ts.start, ts.stop, 0, args...);
+}
+
 void launch_fill_u32(void *p, uint32_t v, long long n, hipStream_t s);
 void launch_fold_stats(const Dev &d, int npart, hipStream_t s);
-void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, hipStream_t s);
-void launch_frame_plan(const Dev &d, const FrameArgs &f, int npart, hipStream_t s);
-void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s);
+// staged_max: upper bound on the scores the previous frame staged (its query
+// count); npart: its scoring blocks whose counts are still to be folded
+void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, int staged_max, int npart,
+                     hipStream_t s, Stamp ts = {});
+void launch_frame_plan(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts = {});
+void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts = {});
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s);
 
 // GRU step for the frame's work list, one launch per layer (max_rows bounds
 // the device-side row count).
-void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s);
+void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s, Stamp ts = {});
 // concatenate W_ih | W_hh of one layer into the packed [3H][Kx+H] layout
 void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_hh, void *dst,
                        hipStream_t s);
 
 
 int lognorm_tiles(int V);
-void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s);
-void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s);
+void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s, Stamp ts = {});
+void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s, Stamp ts = {});
 
 }  // namespace rn

@@ -57,48 +57,74 @@ __device__ __forceinline__ bool nonfinite(float x) {
 // ---------------------------------------------------------------------------
 constexpr int kWordsPerLane = kMaxCW / 64;   // 16
 
-__global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab T) {
-    // enter the scores admitted by the previous frame into the LM-query cache
-    {
-        const long long ns = d.ctr[C_STAGED];
-        const long long step = (long long)gridDim.x * blockDim.x;
-        for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < ns; e += step) {
-            const ScEnt en = d.sc_stage[e];
-            if (en.hs < 0) continue;   // a candidate that turned out to be a cache hit
-            unsigned pos = (unsigned)(query_hash((u64)en.hs, en.w2, en.w3, en.t) & d.si_mask);
-            for (unsigned n = 0; n <= d.si_mask; ++n) {
-                ScEnt *slot = d.sc_tab + pos;
-                if (atomicCAS(&slot->hs, -1, en.hs) == -1) {
-                    slot->w2 = en.w2;
-                    slot->w3 = en.w3;
-                    slot->t = en.t;
-                    slot->val = en.val;
-                    break;
-                }
-                pos = (pos + 1) & d.si_mask;
+// Block roles (independent work, so one launch runs them side by side):
+//   [0, hb)            one wave per history (below)
+//   [hb, hb+qb)        one thread per query: its key, validated
+//   [hb+qb, hb+qb+sb)  enter the scores the previous frame admitted into the
+//                      LM-query cache
+//   last block         fold the previous frame's per-block scoring counts
+//                      into the counters
+__device__ void insert_staged(const Dev &d, int b, int sb) {
+    const long long ns = d.ctr[C_STAGED];
+    for (long long e = (long long)b * blockDim.x + threadIdx.x; e < ns; e += (long long)sb * blockDim.x) {
+        const ScEnt en = d.sc_stage[e];
+        if (en.hs < 0) continue;   // a candidate that turned out to be a cache hit
+        unsigned pos = (unsigned)(query_hash((u64)en.hs, en.w2, en.w3, en.t) & d.si_mask);
+        for (unsigned n = 0; n <= d.si_mask; ++n) {
+            ScEnt *slot = d.sc_tab + pos;
+            if (atomicCAS(&slot->hs, -1, en.hs) == -1) {
+                slot->w2 = en.w2;
+                slot->w3 = en.w3;
+                slot->t = en.t;
+                slot->val = en.val;
+                break;
             }
+            pos = (pos + 1) & d.si_mask;
         }
     }
-    // query keys (history index, MaxEnt context words, target), validated;
-    // input-only work, so it shares this launch with the history waves
-    {
-        const int step = gridDim.x * blockDim.x;
-        unsigned qerr = 0;
-        for (int q = blockIdx.x * blockDim.x + threadIdx.x; q < f.n_query; q += step) {
-            int i = f.q_hist[q];
-            if (i < 0 || i >= f.n_hist) { qerr |= RNNLM_DERR_QHIST; i = 0; }
-            int t = f.q_tgt[q];
-            if (t < 0 || t >= d.V) { qerr |= RNNLM_DERR_WORD; t = 0; }
-            int w[3];
+}
+
+__device__ void query_key(const Dev &d, const FrameArgs &f, int q) {
+    if (q >= f.n_query) return;
+    unsigned qerr = 0;
+    int i = f.q_hist[q];
+    if (i < 0 || i >= f.n_hist) { qerr |= RNNLM_DERR_QHIST; i = 0; }
+    int t = f.q_tgt[q];
+    if (t < 0 || t >= d.V) { qerr |= RNNLM_DERR_WORD; t = 0; }
+    int w[3];
 #pragma unroll
-            for (int c = 0; c < 3; ++c) {   // same clamping as the history waves
-                w[c] = f.hist_words[(size_t)i * 3 + c];
-                if (w[c] < 0 || w[c] >= d.V) w[c] = 0;
-            }
-            d.f_qkey[q] = make_int4(i, d.me_order >= 3 ? w[1] : -1, d.me_order >= 4 ? w[2] : -1, t);
-            d.f_qw1[q] = w[0];
-        }
-        if (qerr) atomicOr(d.derr, qerr);
+    for (int c = 0; c < 3; ++c) {   // same clamping as the history waves
+        w[c] = f.hist_words[(size_t)i * 3 + c];
+        if (w[c] < 0 || w[c] >= d.V) w[c] = 0;
+    }
+    d.f_qkey[q] = make_int4(i, d.me_order >= 3 ? w[1] : -1, d.me_order >= 4 ? w[2] : -1, t);
+    d.f_qw1[q] = w[0];
+    if (qerr) atomicOr(d.derr, qerr);
+}
+
+__device__ void fold_counts(const Dev &d, int npart) {
+    __shared__ int s_red[4];
+    __shared__ long long c[C_N];
+    if (threadIdx.x < C_N) c[threadIdx.x] = d.ctr[threadIdx.x];
+    __syncthreads();
+    fold_partials(d, npart, c, s_red);
+    if (threadIdx.x == 0) {   // only the fields the fold changes
+        d.ctr[C_COMPUTED] = c[C_COMPUTED];
+        d.ctr[C_QUERY_DUPS] = c[C_QUERY_DUPS];
+        d.ctr[C_SCORE_HITS] = c[C_SCORE_HITS];
+        d.ctr[C_SCORE_INS] = c[C_SCORE_INS];
+        d.ctr[C_SC_SIZE] = c[C_SC_SIZE];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab T, int hb, int qb, int sb,
+                                                  int npart) {
+    const int b = blockIdx.x;
+    if (b >= hb) {
+        if (b < hb + qb) query_key(d, f, (b - hb) * blockDim.x + threadIdx.x);
+        else if (b < hb + qb + sb) insert_staged(d, b - hb - qb, sb);
+        else fold_counts(d, npart);
+        return;
     }
     const int lane = threadIdx.x & 63;
     const int i = blockIdx.x * 4 + wave_id();
@@ -258,8 +284,11 @@ void launch_fold_stats(const Dev &d, int npart, hipStream_t s) {
     k_fold_stats<<<1, 256, 0, s>>>(d, npart);
 }
 
-void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, hipStream_t s) {
-    k_hist_key<<<(f.n_hist + 3) / 4, 256, 0, s>>>(d, f, T);
+void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, int staged_max, int npart,
+                     hipStream_t s, Stamp ts) {
+    const int hb = (f.n_hist + 3) / 4, qb = (f.n_query + 255) / 256;
+    const int sb = staged_max > 0 ? (staged_max + 255) / 256 : 0;
+    launch_k(k_hist_key, hb + qb + sb + 1, 256, s, ts, d, f, T, hb, qb, sb, npart);
 }
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s) {

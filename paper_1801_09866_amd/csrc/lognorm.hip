@@ -131,12 +131,12 @@ __global__ __launch_bounds__(256) void k_lognorm_combine(Dev d, int NT, float *l
     if (tid == 0) logz[row] = s[0].x + logf(s[0].y);
 }
 
-void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s) {
-    k_lognorm_gemm<<<lognorm_tiles(d.V), 512, 0, s>>>(d, h, n);
+void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s, Stamp ts) {
+    launch_k(k_lognorm_gemm, lognorm_tiles(d.V), 512, s, ts, d, h, n);
 }
 
-void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s) {
-    k_lognorm_combine<<<n, 256, 0, s>>>(d, lognorm_tiles(d.V), logz);
+void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s, Stamp ts) {
+    launch_k(k_lognorm_combine, n, 256, s, ts, d, lognorm_tiles(d.V), logz);
 }
 
 }  // namespace rn

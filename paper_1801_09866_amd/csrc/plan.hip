@@ -9,9 +9,8 @@
 //              cache itself is probed by the scorer.
 // History keys meet in an LDS hash table on their 64-bit key hash, and a
 // table match is confirmed by comparing codes, so a collision can only cost
-// time. Equal query keys always share a history representative, so queries
-// are bucketed by representative (an LDS counting sort) and compared exactly
-// within their bucket: no hashing at all.
+// time. Query keys meet in a second table on a 32-bit fingerprint, again
+// confirmed by an exact key comparison.
 // Memory discipline: every input is loaded in one round of independent,
 // coalesced loads; the middle of the kernel is LDS work (plus a load for each
 // rare duplicate check); all results are stored at the end. This keeps the
@@ -24,8 +23,13 @@ namespace rn {
 constexpr int PT = 1024;                           // threads
 constexpr int HR = kPlanMaxHist / PT;              // histories per thread at most
 constexpr int QR = kPlanMaxQuery / PT;             // queries per thread at most
-constexpr int TAB_BYTES = 3 * kPlanMaxQuery * 4;    // 96 KB: history table, then query keys
-static_assert(4 * kPlanMaxHist * 12 <= TAB_BYTES, "history table does not fit");
+constexpr int TAB_BYTES = 124 * 1024;              // both hash tables
+constexpr int HW = kPlanMaxHist / 64;              // history flag words
+constexpr int QW = kPlanMaxQuery / 64;             // query flag words
+// worst case: history table at load 1/2 and the query table at load <= 8/9
+static_assert(2 * kPlanMaxHist * 12 + (kPlanMaxQuery + kPlanMaxQuery / 8) * 8 <= TAB_BYTES,
+              "hash tables do not fit");
+static_assert(QW <= 128, "flag prefix covers two words per lane");
 
 __device__ bool same_hist_key(const Dev &d, int a, int b) {
     if (d.f_words[a * 3] != d.f_words[b * 3]) return false;
@@ -35,50 +39,58 @@ __device__ bool same_hist_key(const Dev &d, int a, int b) {
     return true;
 }
 
-// exclusive scan of one int per thread across the block; *total = block sum
-__device__ int block_scan(int v, int *s_tmp, int *total) {
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
-    }
-    if (lane == 63) s_tmp[wv] = x;
-    __syncthreads();
-    if (tid < 16) {
-        int t = s_tmp[tid];
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-            const int y = __shfl_up(t, o, 16);
-            if (tid >= o) t += y;
-        }
-        s_tmp[16 + tid] = t;
-    }
-    __syncthreads();
-    const int base = wv ? s_tmp[16 + wv - 1] : 0;
-    *total = s_tmp[31];
-    __syncthreads();
-    return base + x - v;
-}
-
 // wave-aggregated increment of an LDS counter by the number of lanes with p
 __device__ __forceinline__ void count_lanes(int *ctr, bool p) {
     const int k = __popcll(__ballot(p));
     if ((threadIdx.x & 63) == 0 && k) atomicAdd(ctr, k);
 }
 
-__global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart) {
+// Ranks from flag words: element e (e = r * PT + 64 * wave + lane) sets bit
+// lane of word e / 64 with a wave ballot; one wave then turns the words' bit
+// counts into an exclusive prefix (two words per lane), so the rank of e is
+// pre[e / 64] + the set bits below it in its word. Returns the total (in
+// every lane of the calling wave).
+__device__ int flag_prefix(const u64 *words, int *pre, int nw) {
+    const int lane = threadIdx.x & 63;
+    const int w0 = 2 * lane, w1 = w0 + 1;
+    const int c0 = w0 < nw ? __popcll(words[w0]) : 0, c1 = w1 < nw ? __popcll(words[w1]) : 0;
+    int x = c0 + c1;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    const int ex = x - c0 - c1;
+    if (w0 < nw) pre[w0] = ex;
+    if (w1 < nw) pre[w1] = ex + c0;
+    return __shfl(x, 63, 64);
+}
+
+__device__ __forceinline__ int flag_rank(const u64 *words, const int *pre, int e) {
+    const int lane = e & 63;
+    return pre[e >> 6] + __popcll(words[e >> 6] & ((1ull << lane) - 1ull));
+}
+
+// In-frame placement hash of a query key (history representative, context
+// words, target): the key is folded into 64 bits (injective on realistic
+// ranges, and any collision is caught by the exact check) and mixed once.
+__device__ __forceinline__ u64 frame_query_hash(int rep, int w2, int w3, int t) {
+    const u64 x = (((u64)(uint32_t)(t + 1) << 32) | (uint32_t)(w2 + 2)) + (u64)(uint32_t)(w3 + 2) * kPhi +
+                  (u64)(uint32_t)rep * 0xD6E8FEB86659FD93ull;
+    return mix64(x);
+}
+
+__global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
     __shared__ __align__(16) unsigned char s_tab[TAB_BYTES];
     __shared__ int s_rep[kPlanMaxHist];   // representative | status << 16
     __shared__ int s_hsa[kPlanMaxHist];   // cache slot after the frame (-1: not cached)
     __shared__ int s_loc[kPlanMaxHist];   // where h' lives: slot >= 0, or -(work row + 1)
     __shared__ int s_row[kPlanMaxHist];   // GRU work row of a new key (-1 otherwise)
-    __shared__ int s_bcnt[kPlanMaxHist];  // queries per representative, then bucket offsets
-    __shared__ unsigned short s_bq[kPlanMaxQuery];   // queries grouped by representative
+    __shared__ u64 s_hflag[HW], s_qflag[QW];
+    __shared__ int s_hpre[HW], s_qpre[QW];
     __shared__ long long c[C_N];          // the counters, read once and written back once
-    __shared__ int s_tmp[32];
-    __shared__ int s_cnt[8];
+    __shared__ int s_cnt[4];
+    __shared__ int s_tot;
 
     const int tid = threadIdx.x, n = f.n_hist, nq = f.n_query;
     const int RQ = (nq + PT - 1) / PT;    // active query rounds (block-uniform)
@@ -86,18 +98,14 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
     // ---------------- one round of independent loads ----------------
     long long ctr_v = 0;
     if (tid < C_N) ctr_v = d.ctr[tid];
-    int4 part = make_int4(0, 0, 0, 0);
-    for (int b = tid; b < npart; b += PT) {
-        const int4 p = d.f_part[b];
-        part.x += p.x; part.y += p.y; part.z += p.z; part.w += p.w;
-    }
     u64 h_hash[HR];
-    int h_slot[HR];
+    int h_slot[HR], h_w1[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
         const int i = min(tid + r * PT, n - 1);   // clamped: no divergent loads
         h_hash[r] = d.f_hhash[i];
         h_slot[r] = d.f_hcslot[i];
+        h_w1[r] = d.f_words[i * 3];
     }
     int4 qk[QR];
     int qw1[QR];
@@ -109,41 +117,33 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
         qw1[r] = d.f_qw1[q];
     }
 
-    // counters and last frame's scoring counts
-    if (tid < C_N) c[tid] = ctr_v;
-    if (tid < 8) s_cnt[tid] = 0;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        part.x += __shfl_xor(part.x, o, 64);
-        part.y += __shfl_xor(part.y, o, 64);
-        part.z += __shfl_xor(part.z, o, 64);
-        part.w += __shfl_xor(part.w, o, 64);
-    }
-    __syncthreads();
-    if ((tid & 63) == 0 && npart) {
-        atomicAdd(&s_cnt[4], part.x);
-        atomicAdd(&s_cnt[5], part.y);
-        atomicAdd(&s_cnt[6], part.z);
-        atomicAdd(&s_cnt[7], part.w);
-    }
-
-    // ---------------- histories ----------------
+    // ---------------- both tables cleared while the loads are in flight ----
+    // history table: 64-bit key hash + lowest index per slot (load <= 1/4 when
+    // both tables fit that way, else 1/2); query table: 32-bit fingerprint +
+    // lowest index per slot, in the rest
     int HT = 64;
-    while (HT < 4 * n) HT <<= 1;   // load <= 1/4: short probe chains
+    while (HT < 4 * n) HT <<= 1;
+    if (HT * 12 + 12 * nq > TAB_BYTES) HT >>= 1;
+    const int TQ = min((TAB_BYTES - HT * 12) / 8, max(64, 4 * nq));
     u64 *hkey = reinterpret_cast<u64 *>(s_tab);
     int *hmin = reinterpret_cast<int *>(s_tab + HT * 8);
+    unsigned *qfp = reinterpret_cast<unsigned *>(s_tab + HT * 12);
+    int *qmin = reinterpret_cast<int *>(s_tab + HT * 12 + TQ * 4);
     for (int e = tid; e < HT; e += PT) {
         hkey[e] = 0ull;
         hmin[e] = 0x7FFFFFFF;
     }
-    __syncthreads();
-    if (tid == 0) {
-        c[C_COMPUTED] += s_cnt[4];
-        c[C_QUERY_DUPS] += s_cnt[5];
-        c[C_SCORE_HITS] += s_cnt[6];
-        c[C_SCORE_INS] += s_cnt[7];
-        c[C_SC_SIZE] += s_cnt[7];
+    if (RQ > 0) {
+        for (int e = tid; e < TQ; e += PT) {
+            qfp[e] = 0u;
+            qmin[e] = 0x7FFFFFFF;
+        }
     }
+    if (tid < C_N) c[tid] = ctr_v;   // the previous frame's scoring counts are already folded in
+    if (tid < 4) s_cnt[tid] = 0;
+    __syncthreads();
+
+    // ---------------- histories ----------------
     unsigned hpos[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
@@ -177,22 +177,38 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
             }
         }
     }
-    // statuses, GRU work rows, history-cache admission (ascending index)
-    const long long hc_size = c[C_HC_SIZE];
-    int carry = 0;
+    // statuses; the GRU work row of a new key is its rank among the frame's
+    // new keys (ascending index), and keys enter the history cache in that
+    // order while it has room
+    int h_st[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
         if (r * PT >= n) break;   // block-uniform
         const int i = tid + r * PT;
         const bool live = i < n;
-        int st = RNNLM_H_DUP;
-        if (live) st = h_slot[r] >= 0 ? RNNLM_HC_HIT : (h_rep[r] == i ? RNNLM_H_REP : RNNLM_H_DUP);
-        int total;
-        const int row = block_scan(live && st == RNNLM_H_REP ? 1 : 0, s_tmp, &total) + carry;
-        const bool adm = live && st == RNNLM_H_REP && hc_size + row < d.cap_hist;
+        h_st[r] = !live ? RNNLM_H_DUP : h_slot[r] >= 0 ? RNNLM_HC_HIT : (h_rep[r] == i ? RNNLM_H_REP : RNNLM_H_DUP);
+        const u64 b = __ballot(live && h_st[r] == RNNLM_H_REP);
+        if ((tid & 63) == 0) s_hflag[i >> 6] = b;
+    }
+    __syncthreads();
+    if (tid < 64) {
+        const int tot = flag_prefix(s_hflag, s_hpre, (n + 63) >> 6);
+        if (tid == 0) s_tot = tot;
+    }
+    __syncthreads();
+    const long long hc_size = c[C_HC_SIZE];
+    const int M = s_tot;
+#pragma unroll
+    for (int r = 0; r < HR; ++r) {
+        if (r * PT >= n) break;   // block-uniform
+        const int i = tid + r * PT;
+        const bool live = i < n;
+        const int st = h_st[r];
+        const int row = live && st == RNNLM_H_REP ? flag_rank(s_hflag, s_hpre, i) : -1;
+        const bool adm = row >= 0 && hc_size + row < d.cap_hist;
         if (live) {
             s_rep[i] = h_rep[r] | (st << 16);
-            s_row[i] = st == RNNLM_H_REP ? row : -1;
+            s_row[i] = row;
             if (st == RNNLM_HC_HIT) {
                 s_hsa[i] = h_slot[r];
                 s_loc[i] = h_slot[r];
@@ -203,160 +219,117 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
         }
         count_lanes(&s_cnt[0], live && st == RNNLM_HC_HIT);
         count_lanes(&s_cnt[1], live && st == RNNLM_H_DUP);
-        count_lanes(&s_cnt[2], adm);
-        count_lanes(&s_cnt[3], live && st == RNNLM_H_REP && !adm);
-        carry += total;
     }
     __syncthreads();
     // duplicates share their representative's h' and cache slot
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
         const int i = tid + r * PT;
-        if (i < n && (s_rep[i] >> 16) == RNNLM_H_DUP) {
+        if (i < n && h_st[r] == RNNLM_H_DUP) {
             s_hsa[i] = s_hsa[h_rep[r]];
             s_loc[i] = s_loc[h_rep[r]];
         }
     }
     if (tid == 0) {
-        c[C_FRAME_M] = carry;
-        c[C_HC_SIZE] = hc_size + s_cnt[2];
+        const long long room = d.cap_hist > hc_size ? d.cap_hist - hc_size : 0;
+        const int ins = (int)(M < room ? M : room);
+        c[C_FRAME_M] = M;
+        c[C_HC_SIZE] = hc_size + ins;
         c[C_FRAMES] += 1;
         c[C_HISTS] += n;
         c[C_HIST_HITS] += s_cnt[0];
         c[C_HIST_DUPS] += s_cnt[1];
-        c[C_GRU_ROWS] += carry;
-        c[C_HIST_INS] += s_cnt[2];
-        c[C_HIST_REJ] += s_cnt[3];
+        c[C_GRU_ROWS] += M;
+        c[C_HIST_INS] += ins;
+        c[C_HIST_REJ] += M - ins;
         c[C_QUERIES] += nq;
         c[C_STAGED] = 0;   // the keys kernel has entered last frame's admitted scores
         c[C_NEAR_CAP] = 0;
     }
 
     // ---------------- queries ----------------
+    // Query keys meet on a 32-bit fingerprint; each slot keeps the lowest
+    // query index that reached it, and a match is confirmed against that
+    // query's exact key (on a fingerprint collision the query scans the
+    // earlier queries itself, which stays exact).
     if (RQ > 0) {
-        int *s_qt = reinterpret_cast<int *>(s_tab);          // target
-        int *s_qw2 = s_qt + kPlanMaxQuery;                    // key context words
-        int *s_qw3 = s_qw2 + kPlanMaxQuery;
-        for (int e = tid; e < n; e += PT) s_bcnt[e] = 0;
-        __syncthreads();   // history table dead; duplicates' fix-up ordered
-        // count the queries of each representative; the count's old value is
-        // the query's place in its bucket
-        int slot[QR];
+        int qrh[QR];          // the query's history representative
+        unsigned qpos[QR];
 #pragma unroll
         for (int r = 0; r < QR; ++r) {
             const int q = tid + r * PT;
             if (r < RQ && q < nq) {
-                s_qt[q] = qk[r].w;
-                s_qw2[q] = qk[r].y;
-                s_qw3[q] = qk[r].z;
-                slot[r] = atomicAdd(&s_bcnt[s_rep[qk[r].x] & 0xFFFF], 1);
+                qrh[r] = s_rep[qk[r].x] & 0xFFFF;
+                const u64 h = frame_query_hash(qrh[r], qk[r].y, qk[r].z, qk[r].w);
+                const unsigned fp = (unsigned)(h >> 32) | 1u;
+                unsigned pos = (unsigned)(((h & 0xFFFFFFFFull) * (u64)TQ) >> 32);
+                for (int k = 0; k < TQ; ++k) {
+                    const unsigned old = atomicCAS(&qfp[pos], 0u, fp);
+                    if (old == 0u || old == fp) { atomicMin(&qmin[pos], q); break; }
+                    if (++pos == (unsigned)TQ) pos = 0;
+                }
+                qpos[r] = pos;
             }
         }
-        __syncthreads();
-        // bucket offsets: exclusive scan of the counts in representative order
-        int carry2 = 0;
-        for (int c0 = 0; c0 < n; c0 += PT) {
-            const int e = c0 + tid;
-            const int v = e < n ? s_bcnt[e] : 0;
-            int total;
-            const int off = block_scan(v, s_tmp, &total) + carry2;
-            if (e < n) s_bcnt[e] = off;
-            carry2 += total;
-        }
-        __syncthreads();
+        __syncthreads();   // also orders the duplicates' fix-up
+        int qrepv[QR];
 #pragma unroll
         for (int r = 0; r < QR; ++r) {
             const int q = tid + r * PT;
-            if (r < RQ && q < nq) s_bq[s_bcnt[s_rep[qk[r].x] & 0xFFFF] + slot[r]] = (unsigned short)q;
-        }
-        __syncthreads();
-        // one thread per bucket: representative = lowest query index with the
-        // same (context, target) among the bucket's queries. The bucket's keys
-        // are read once; each query's representative then replaces its target
-        // in s_qt (only this thread touches the bucket's entries).
-        constexpr int KB = 8;    // bucket entries held in registers
-        for (int hr = tid; hr < n; hr += PT) {
-            const int b0 = s_bcnt[hr], b1 = hr + 1 < n ? s_bcnt[hr + 1] : nq;
-            const int k = b1 - b0;
-            if (k == 0) continue;
-            if (k <= KB) {
-                int bq[KB], bt[KB], b2[KB], b3[KB];
-#pragma unroll
-                for (int j = 0; j < KB; ++j) {
-                    if (j < k) {
-                        bq[j] = s_bq[b0 + j];
-                        bt[j] = s_qt[bq[j]];
-                        b2[j] = s_qw2[bq[j]];
-                        b3[j] = s_qw3[bq[j]];
+            qrepv[r] = q;
+            if (r < RQ && q < nq) {
+                const int m = qmin[qpos[r]];
+                if (m != q) {
+                    const int4 km = d.f_qkey[m];
+                    if ((s_rep[km.x] & 0xFFFF) == qrh[r] && km.y == qk[r].y && km.z == qk[r].z && km.w == qk[r].w) {
+                        qrepv[r] = m;
+                    } else {
+                        for (int j = 0; j < q; ++j) {
+                            const int4 kj = d.f_qkey[j];
+                            if ((s_rep[kj.x] & 0xFFFF) == qrh[r] && kj.y == qk[r].y && kj.z == qk[r].z &&
+                                kj.w == qk[r].w) {
+                                qrepv[r] = j;
+                                break;
+                            }
+                        }
                     }
-                }
-#pragma unroll
-                for (int j = 0; j < KB; ++j) {
-                    if (j < k) {
-                        int rep = bq[j];
-#pragma unroll
-                        for (int l = 0; l < KB; ++l)
-                            if (l < k && bq[l] < rep && bt[l] == bt[j] && b2[l] == b2[j] && b3[l] == b3[j]) rep = bq[l];
-                        s_qt[bq[j]] = rep;   // own entries only; keys were read above
-                    }
-                }
-            } else {   // a large bucket, in LDS: sort it by query index, then resolve
-                       // from the back, so each write lands on an entry no later
-                       // comparison reads
-                for (int j = 1; j < k; ++j) {
-                    const unsigned short v = s_bq[b0 + j];
-                    int l = j - 1;
-                    while (l >= 0 && s_bq[b0 + l] > v) {
-                        s_bq[b0 + l + 1] = s_bq[b0 + l];
-                        --l;
-                    }
-                    s_bq[b0 + l + 1] = v;
-                }
-                for (int j = k - 1; j >= 0; --j) {
-                    const int qj = s_bq[b0 + j];
-                    int rep = qj;
-                    for (int l = 0; l < j; ++l) {
-                        const int ql = s_bq[b0 + l];
-                        if (s_qt[ql] == s_qt[qj] && s_qw2[ql] == s_qw2[qj] && s_qw3[ql] == s_qw3[qj]) { rep = ql; break; }
-                    }
-                    s_qt[qj] = rep;
                 }
             }
         }
-        __syncthreads();
-        const long long sc_size = c[C_SC_SIZE];
-        int qcarry = 0;
-        int qrep[QR];
+        // a new key whose history is (or will be) cached may enter the
+        // LM-query cache; candidates are ranked in query order
 #pragma unroll
         for (int r = 0; r < QR; ++r) {
             if (r >= RQ) break;   // block-uniform
             const int q = tid + r * PT;
-            int rep = q;
-            bool cand = false;
-            if (q < nq) {
-                rep = s_qt[q];
-                cand = rep == q && s_hsa[qk[r].x] >= 0;   // may enter the LM-query cache
-            }
-            int total;
-            const int rank = block_scan(cand ? 1 : 0, s_tmp, &total) + qcarry;
-            qrep[r] = rep | (cand ? (rank << 16) : (int)0x80000000);   // rep, rank < 2^15
-            qcarry += total;
+            const bool cand = q < nq && qrepv[r] == q && s_hsa[qk[r].x] >= 0;
+            const u64 b = __ballot(cand);
+            if ((tid & 63) == 0) s_qflag[q >> 6] = b;
         }
+        __syncthreads();
+        if (tid < 64) {
+            const int tot = flag_prefix(s_qflag, s_qpre, (nq + 63) >> 6);
+            if (tid == 0) s_tot = tot;
+        }
+        __syncthreads();
+        const int ncand = s_tot;
+        const long long sc_size = c[C_SC_SIZE];
         // scorer records
 #pragma unroll
         for (int r = 0; r < QR; ++r) {
             const int q = tid + r * PT;
             if (r < RQ && q < nq) {
                 const int i = qk[r].x;
-                const int rep = qrep[r] & 0xFFFF;
-                const bool cand = qrep[r] >= 0;
+                const int rep = qrepv[r];
+                const bool cand = (s_qflag[q >> 6] >> (q & 63)) & 1ull;
+                const int rank = cand ? flag_rank(s_qflag, s_qpre, q) : 0;
                 const int loc = s_loc[i];
                 const float *base = loc >= 0 ? d.hc_val + (size_t)loc * d.LH : d.f_hval + (size_t)(-loc - 1) * d.LH;
                 QRec rec;
                 rec.hptr = (u64)(base + (size_t)(d.L - 1) * d.H);
                 rec.t = qk[r].w;
                 rec.flags = (rep < q ? RNNLM_Q_DUP : RNNLM_Q_COMPUTED) | (cand ? QF_CAND : 0) |
-                            ((s_rep[i] >> 16) == RNNLM_HC_HIT ? QF_PROBE : 0) | (cand ? (qrep[r] >> 16) << 6 : 0);
+                            ((s_rep[i] >> 16) == RNNLM_HC_HIT ? QF_PROBE : 0) | (cand ? rank << 6 : 0);
                 rec.hs = s_hsa[i];
                 rec.w1 = qw1[r];
                 rec.w2 = qk[r].y;
@@ -367,9 +340,9 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
         }
         if (tid == 0) {
             // admission is order-independent unless the candidates could overflow the cache
-            const bool near = sc_size + qcarry > d.cap_query;
+            const bool near = sc_size + ncand > d.cap_query;
             c[C_NEAR_CAP] = near ? 1 : 0;
-            c[C_STAGED] = near ? 0 : qcarry;   // staging slots the scorer fills
+            c[C_STAGED] = near ? 0 : ncand;   // staging slots the scorer fills
         }
     }
 
@@ -387,6 +360,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
             if (st == RNNLM_H_REP) {
                 const int row = s_row[i];
                 d.f_rows[row] = i;
+                d.f_roww[row] = h_w1[r];
                 d.f_rowdst[row] = (u64)hp;
             }
             if (f.h_status) f.h_status[i] = (uint8_t)st;
@@ -397,8 +371,8 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f, int npart
     if (tid < C_N) d.ctr[tid] = c[tid];
 }
 
-void launch_frame_plan(const Dev &d, const FrameArgs &f, int npart, hipStream_t s) {
-    k_frame_plan<<<1, PT, 0, s>>>(d, f, npart);
+void launch_frame_plan(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts) {
+    launch_k(k_frame_plan, 1, PT, s, ts, d, f);
 }
 
 }  // namespace rn

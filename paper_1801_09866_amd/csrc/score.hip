@@ -210,12 +210,12 @@ __global__ __launch_bounds__(256) void k_score_finish(Dev d, FrameArgs f, int qb
     if (tid == 0) d.ctr[C_DONE] = 0;
 }
 
-void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s) {
+void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts) {
     const int qb = (f.n_query + 3) / 4, hb = (f.n_hist + 3) / 4;
     if (d.wdtype == RNNLM_BF16)
-        k_score_finish<true><<<qb + hb, 256, 0, s>>>(d, f, qb);
+        launch_k(k_score_finish<true>, qb + hb, 256, s, ts, d, f, qb);
     else
-        k_score_finish<false><<<qb + hb, 256, 0, s>>>(d, f, qb);
+        launch_k(k_score_finish<false>, qb + hb, 256, s, ts, d, f, qb);
 }
 
 }  // namespace rn
