@@ -16,6 +16,12 @@ Per frame, in order (one call of ``Oracle.score_frame``):
   5. one GRU step per history key not in the cache       (Sec. 2.1)
   6. unnormalised NCE score + hashed n-gram MaxEnt terms  (Sec. 2.2, 2.3)
   7. insert the frame's new keys into the two caches     (Sec. 2.4, Sec. 3)
+
+Parity unpinned: the compositions in ``hist_key_hash`` and ``maxent_index``
+are this implementation's own definitions, because the paper leaves both
+hashes unspecified (Sec. 2.3, Sec. 3). Only their building block, the
+SplitMix64 finaliser ``mix64``, is pinned, by its published outputs; nothing
+outside this file fixes how the finaliser is combined.
 """
 from __future__ import annotations
 
