@@ -112,175 +112,10 @@ __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
     return r;
 }
 
-// ------------------------ skinny path (few rows) --------------------------
-// In steady state most history keys are cached and a frame has only a few new
-// keys. Then the weights (not the FLOPs) are the cost: each block takes 4
-// hidden units (12 packed weight rows) for every row; its 8 waves split into
-// 4 units x 2 halves of K, with the rows' [x ; h] staged in LDS once per
-// block. Blocks are dealt to XCDs so that each XCD streams a contiguous 1/8
-// of the weights.
-constexpr int S_UNITS = 4;          // hidden units per block
-constexpr int S_MAXROWS = 16;       // rows handled by the skinny path at most
-constexpr int S_CHUNKS = 16;        // 64-wide K chunks whose weights a wave fetches at once
-constexpr int S_LDS_FLOATS = 24576; // 96 KB LDS buffer shared with the MFMA path
-constexpr int S_PART = 4 * 4 * S_MAXROWS;               // second-half partial sums
-constexpr int S_A_FLOATS = S_LDS_FLOATS - S_PART;       // staged rows
+// One LDS buffer serves every path.
+constexpr int G_LDS_FLOATS = 24576;   // 96 KB
 
-__device__ __forceinline__ int skinny_rows(int K) {
-    const int r = S_A_FLOATS / K;
-    return r < S_MAXROWS ? r : S_MAXROWS;
-}
-
-template <bool BF16W>
-__device__ void gru_skinny(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int b) {
-    const int NB = d.H / S_UNITS;
-    const int g = (NB & 7) == 0 ? (b & 7) * (NB >> 3) + (b >> 3) : b;
-    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
-    const int Kx = layer == 0 ? d.E : d.H;
-    const int K = Kx + d.H;
-    float *sA = smem;
-    float *sP = smem + S_A_FLOATS;
-
-    // the M rows' sources, resolved once, in parallel
-    __shared__ const void *s_x[S_MAXROWS];
-    __shared__ const float *s_h[S_MAXROWS];
-    __shared__ float *s_dst[S_MAXROWS];
-    if (tid < M) {
-        const RowSrc src = row_source(d, f, layer, tid, M);
-        s_x[tid] = src.x;
-        s_h[tid] = src.h;
-        s_dst[tid] = reinterpret_cast<float *>(d.f_rowdst[tid]) + (size_t)layer * d.H;
-    }
-    __syncthreads();
-    // stage the rows [x ; h] (bf16 weights: rows rounded to bf16, as the MFMA
-    // path does); SB float4 per thread are in flight at once
-    const bool xbf = layer == 0 && BF16W;
-    const int K4 = K / 4, n4 = M * K4;
-    constexpr int SB = 8;
-    for (int e0 = tid; e0 < n4; e0 += G_THREADS * SB) {
-        float4 v[SB];
-#pragma unroll
-        for (int q = 0; q < SB; ++q) {
-            const int e = e0 + q * G_THREADS;
-            if (e < n4) {
-                const int m = e / K4, k = (e - m * K4) * 4;
-                if (k < Kx) {
-                    if (xbf) {
-                        const uint2 u2 = *reinterpret_cast<const uint2 *>(reinterpret_cast<const uint16_t *>(s_x[m]) + k);
-                        v[q] = make_float4(__uint_as_float(u2.x << 16), __uint_as_float(u2.x & 0xFFFF0000u),
-                                           __uint_as_float(u2.y << 16), __uint_as_float(u2.y & 0xFFFF0000u));
-                    } else {
-                        v[q] = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(s_x[m]) + k);
-                    }
-                } else {
-                    v[q] = *reinterpret_cast<const float4 *>(s_h[m] + (k - Kx));
-                }
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < SB; ++q) {
-            const int e = e0 + q * G_THREADS;
-            if (e < n4) {
-                float4 x = v[q];
-                if (BF16W) {
-                    x.x = bf16_to_f32(f32_to_bf16(x.x));
-                    x.y = bf16_to_f32(f32_to_bf16(x.y));
-                    x.z = bf16_to_f32(f32_to_bf16(x.z));
-                    x.w = bf16_to_f32(f32_to_bf16(x.w));
-                }
-                *reinterpret_cast<float4 *>(sA + e * 4) = x;   // row m at m * K
-            }
-        }
-    }
-    __syncthreads();
-
-    const int u = w & 3, half = w >> 2;
-    const int j = g * S_UNITS + u;
-    const size_t rr = (size_t)j * K, rz = (size_t)(d.H + j) * K, rn_ = (size_t)(2 * d.H + j) * K;
-    float ar[S_MAXROWS], az[S_MAXROWS], anx[S_MAXROWS], anh[S_MAXROWS];
-#pragma unroll
-    for (int m = 0; m < S_MAXROWS; ++m) ar[m] = az[m] = anx[m] = anh[m] = 0.0f;
-    auto wload = [&](size_t off) -> float {
-        if (BF16W) return bf16_to_f32(reinterpret_cast<const uint16_t *>(d.Wp[layer])[off]);
-        return reinterpret_cast<const float *>(d.Wp[layer])[off];
-    };
-    // 64-wide chunks of K; the first half of the chunks to waves 0-3, the rest
-    // to 4-7. All of a wave's weights are fetched at once (one memory round
-    // trip); the candidate gate's weight is split per chunk into its input and
-    // recurrent parts, so the row loop below has no branch. Rows go in groups
-    // of 4 and chunks in batches of 4: each (group, batch) issues its 16 LDS
-    // reads together.
-    const int nc = K / 64, h0 = half ? nc / 2 : 0, c1 = half ? nc : nc / 2;
-    for (int c0 = h0; c0 < c1; c0 += S_CHUNKS) {   // S_CHUNKS chunks per pass
-        float wr[S_CHUNKS], wz[S_CHUNKS], wnx[S_CHUNKS], wnh[S_CHUNKS];
-#pragma unroll
-        for (int u2 = 0; u2 < S_CHUNKS; ++u2) {
-            const int c = c0 + u2;
-            const int k = c * 64 + lane;
-            const bool ok = c < c1;
-            wr[u2] = ok ? wload(rr + k) : 0.0f;
-            wz[u2] = ok ? wload(rz + k) : 0.0f;
-            const float wn = ok ? wload(rn_ + k) : 0.0f;
-            const bool xpart = c * 64 < Kx;   // chunk-uniform
-            wnx[u2] = xpart ? wn : 0.0f;
-            wnh[u2] = xpart ? 0.0f : wn;
-        }
-#pragma unroll
-        for (int g = 0; g < S_MAXROWS / 4; ++g) {
-            if (4 * g >= M) break;   // block-uniform
-#pragma unroll
-            for (int cb = 0; cb < S_CHUNKS; cb += 4) {
-                if (c0 + cb >= c1) break;   // wave-uniform
-                float a[4][4];
-#pragma unroll
-                for (int u2 = 0; u2 < 4; ++u2) {
-                    const int k = min(c0 + cb + u2, c1 - 1) * 64 + lane;   // padded chunks: weight 0
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) a[u2][r] = sA[min(4 * g + r, M - 1) * K + k];
-                }
-#pragma unroll
-                for (int u2 = 0; u2 < 4; ++u2) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int m = 4 * g + r;
-                        ar[m] = fmaf(a[u2][r], wr[cb + u2], ar[m]);
-                        az[m] = fmaf(a[u2][r], wz[cb + u2], az[m]);
-                        anx[m] = fmaf(a[u2][r], wnx[cb + u2], anx[m]);
-                        anh[m] = fmaf(a[u2][r], wnh[cb + u2], anh[m]);
-                    }
-                }
-            }
-        }
-    }
-    // full sums in every lane; lane m then owns row m
-    float vr = 0.0f, vz = 0.0f, vnx = 0.0f, vnh = 0.0f;
-#pragma unroll
-    for (int m = 0; m < S_MAXROWS; ++m) {
-        if (m < M) {
-            const float sr = wave_sum(ar[m]), sz = wave_sum(az[m]), snx = wave_sum(anx[m]), snh = wave_sum(anh[m]);
-            if (lane == m) {
-                vr = sr;
-                vz = sz;
-                vnx = snx;
-                vnh = snh;
-            }
-        }
-    }
-    float4 *sP4 = reinterpret_cast<float4 *>(sP) + u * S_MAXROWS;
-    if (half && lane < M) sP4[lane] = make_float4(vr, vz, vnx, vnh);
-    __syncthreads();
-    if (half || lane >= M) return;   // the caller's next tile starts with a barrier
-    const float *bb = d.b_ih[layer];
-    const float br = bb[j], bz = bb[d.H + j], bn = bb[2 * d.H + j];
-    const float hprev = s_h[lane][j];
-    const float4 p = sP4[lane];
-    const float r = sigmoidf_(vr + p.x + br);
-    const float z = sigmoidf_(vz + p.y + bz);
-    const float n = tanhf(vnx + p.z + bn + r * (vnh + p.w));
-    s_dst[lane][j] = (1.0f - z) * n + z * hprev;
-}
-
-// ------------------------ medium path (16 < rows <= 256) -------------------
+// ------------------------ medium path (32 < rows <= 256) -------------------
 // Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
 // accumulating the four gate tiles (reset, update, candidate input part,
 // candidate recurrent part) of its K range with MFMAs fed straight from
@@ -404,6 +239,131 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
             gru_epilogue(d, f, layer, M, m0, j0, 0, 0, ar, az, anx, anh);
         }
         __syncthreads();   // the partial tiles are reused by the next tile
+    }
+}
+
+// ------------------------ narrow path (few rows) ---------------------------
+// A frame with few new keys is bound by reading the weights once and by
+// memory latency, not by FLOPs. Every block owns 4 hidden units for all rows,
+// so all 256 CUs share the weight stream (each XCD its own contiguous 1/8,
+// which stays in its L2). One 16 x 16 MFMA tile holds the block's 12 gate
+// columns (r, z, n of 4 units; 4 columns padding) for 16 rows; the 8 waves
+// split K, each keeping an input-part and a recurrent-part accumulator per
+// row tile (the candidate gate needs them apart), and issue all of a pass's
+// operand loads at once. The partial tiles meet in LDS in a fixed order, and
+// one thread per (row, unit) applies the gates with operands it loaded before
+// the K loop.
+constexpr int N_MAXROWS = 32;   // rows handled by the narrow path at most
+constexpr int N_TILES = N_MAXROWS / 16;
+
+template <bool BF16W>
+__device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int g) {
+    using T = typename MdOps<BF16W>::T;
+    using E = typename std::conditional<BF16W, uint16_t, float>::type;
+    constexpr int KS = BF16W ? 32 : 16;   // k per step
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H, K = Kx + d.H;
+    const int nsteps = K / KS;
+    const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;   // scalars
+    const int col = lane & 15, kq = (KS / 4) * (lane >> 4);
+    const int gate = col >> 2, j0 = 4 * g;
+    const bool wcol = gate < 3;           // padding columns multiply zeros
+    const E *wrow = reinterpret_cast<const E *>(d.Wp[layer]) + (size_t)((wcol ? gate : 0) * d.H + j0 + (col & 3)) * K + kq;
+    const int nt = (M + 15) >> 4;         // row tiles (block-uniform)
+
+    // epilogue operands of thread (row m, unit u), loaded before the K loop
+    const int em = tid >> 2, eu = tid & 3;
+    const bool eth = em < M;
+    float ebr = 0.f, ebz = 0.f, ebn = 0.f, ehp = 0.f;
+    float *edst = nullptr;
+    if (eth) {
+        const int j = j0 + eu;
+        const float *bb = d.b_ih[layer];
+        ebr = bb[j];
+        ebz = bb[d.H + j];
+        ebn = bb[2 * d.H + j];
+        const int i = d.f_rows[em];
+        edst = reinterpret_cast<float *>(d.f_rowdst[em]) + (size_t)layer * d.H + j;
+        ehp = f.hist_vec[(size_t)i * d.LH + (size_t)layer * d.H + j];
+    }
+    constexpr int PASS = 12;              // steps whose operands are loaded together
+    T b[PASS];
+    RowSrc src[N_TILES];
+#pragma unroll
+    for (int t = 0; t < N_TILES; ++t) src[t] = row_source(d, f, layer, 16 * t + col, M);
+
+    auto loadA = [&](const RowSrc &rs, int k) -> T {
+        if (!rs.valid) return T{0, 0, 0, 0};
+        if (!BF16W) {
+            const float *p = k < Kx ? reinterpret_cast<const float *>(rs.x) + k : rs.h + (k - Kx);
+            return __builtin_bit_cast(T, *reinterpret_cast<const float4 *>(p));
+        }
+        if (k < Kx && rs.x_bf16)
+            return __builtin_bit_cast(T, *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(rs.x) + k));
+        const float *p = k < Kx ? reinterpret_cast<const float *>(rs.x) + k : rs.h + (k - Kx);
+        return __builtin_bit_cast(T, pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4)));
+    };
+
+    f4_t accx[N_TILES], acch[N_TILES];
+#pragma unroll
+    for (int t = 0; t < N_TILES; ++t) accx[t] = acch[t] = f4_t{0, 0, 0, 0};
+    for (int p0 = s0; p0 < s1; p0 += PASS) {
+        T a[N_TILES][PASS];
+#pragma unroll
+        for (int c = 0; c < PASS; ++c) {
+            const int st = p0 + c;
+            if (st < s1) {   // wave-uniform
+                const int k = st * KS;
+                b[c] = wcol ? *reinterpret_cast<const T *>(wrow + k) : T{0, 0, 0, 0};
+#pragma unroll
+                for (int t = 0; t < N_TILES; ++t)
+                    if (t < nt) a[t][c] = loadA(src[t], k + kq);
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < PASS; ++c) {
+            const int st = p0 + c;
+            if (st < s1) {
+                const bool xp = st * KS < Kx;   // wave-uniform
+#pragma unroll
+                for (int t = 0; t < N_TILES; ++t) {
+                    if (t < nt) {
+                        if (xp) accx[t] = md_mfma(a[t][c], b[c], accx[t]);
+                        else acch[t] = md_mfma(a[t][c], b[c], acch[t]);
+                    }
+                }
+            }
+        }
+    }
+    // partial tiles to LDS: [wave][tile][part][lane][4]
+#pragma unroll
+    for (int t = 0; t < N_TILES; ++t) {
+        if (t < nt) {
+            float *px = smem + ((size_t)((w * N_TILES + t) * 2 + 0) * 64 + lane) * 4;
+            float *ph = smem + ((size_t)((w * N_TILES + t) * 2 + 1) * 64 + lane) * 4;
+            *reinterpret_cast<float4 *>(px) = make_float4(accx[t][0], accx[t][1], accx[t][2], accx[t][3]);
+            *reinterpret_cast<float4 *>(ph) = make_float4(acch[t][0], acch[t][1], acch[t][2], acch[t][3]);
+        }
+    }
+    __syncthreads();
+    if (eth) {
+        // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+        const int t = em >> 4, i = em & 15, e = i & 3, lb = 16 * (i >> 2);
+        float xr = 0.f, xz = 0.f, xn = 0.f, hr = 0.f, hz = 0.f, hn = 0.f;
+        for (int v = 0; v < 8; ++v) {   // fixed order: equal inputs give equal bits
+            const float *px = smem + (size_t)((v * N_TILES + t) * 2 + 0) * 256 + e;
+            const float *ph = smem + (size_t)((v * N_TILES + t) * 2 + 1) * 256 + e;
+            xr += px[(lb + eu) * 4];
+            xz += px[(lb + 4 + eu) * 4];
+            xn += px[(lb + 8 + eu) * 4];
+            hr += ph[(lb + eu) * 4];
+            hz += ph[(lb + 4 + eu) * 4];
+            hn += ph[(lb + 8 + eu) * 4];
+        }
+        const float r = sigmoidf_(xr + hr + ebr);
+        const float z = sigmoidf_(xz + hz + ebz);
+        const float n = tanhf(xn + ebn + r * hn);
+        *edst = (1.0f - z) * n + z * ehp;
     }
 }
 
@@ -579,19 +539,22 @@ __device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M
 }
 
 // One launch per layer; the device-side row count picks the path.
-static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= S_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
-static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= S_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
+static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
+static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles exceed the LDS buffer");
+static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
+static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
 template <bool BF16W>
 __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, FrameArgs f, int layer) {
-    __shared__ __align__(16) float smem[S_LDS_FLOATS];
+    __shared__ __align__(16) float smem[G_LDS_FLOATS];
     const int M = (int)d.ctr[C_FRAME_M];
     if (M <= 0) return;
-    const int K = (layer == 0 ? d.E : d.H) + d.H;
-    if (M <= skinny_rows(K)) {        // few rows: stream the weights through the VALU
-        for (int t = blockIdx.x; t < d.H / S_UNITS; t += gridDim.x) {
+    if (M <= N_MAXROWS) {             // few rows: every CU streams its share of the weights
+        const int NB = d.H / 4;
+        for (int t = blockIdx.x; t < NB; t += gridDim.x) {
+            const int g = (NB & 7) == 0 && (int)gridDim.x >= NB ? (t & 7) * (NB >> 3) + (t >> 3) : t;
             __syncthreads();
-            gru_skinny<BF16W>(d, f, layer, M, smem, t);
+            gru_narrow<BF16W>(d, f, layer, M, smem, g);
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
         gru_medium<BF16W>(d, f, layer, M, smem);

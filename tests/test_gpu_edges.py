@@ -164,13 +164,13 @@ def test_host_rejects_oversized_frames():
 
 @pytest.mark.parametrize("L,wd", [(1, F32), (2, F32), (1, 1)])
 def test_gru_paths_by_row_count(L, wd):
-    """Row counts on each side of the skinny (<= 16), medium (<= 256) and
+    """Row counts on each side of the narrow (<= 32), medium (<= 256) and
     64 x 32 tile paths, all new keys, against the oracle."""
     m = ModelCfg(V=3000, E=128, H=256, L=L, wdtype=wd, maxent_log2=12, maxent_order=4)
     rng = np.random.default_rng(10 + L + 3 * wd)
     w = weights(m, rng, scale=0.08)
     tol = (2e-2, 0.0) if wd == 1 else (ATOL, RTOL)
-    for n_h in (1, 15, 16, 17, 64, 200, 256, 257, 512):
+    for n_h in (1, 15, 16, 17, 32, 33, 64, 200, 256, 257, 512):
         b = Both(m, w, Q_EXACT, max_hist=512, max_query=1024)
         vec, words, qh, qt = rand_frame(rng, m, n_h, min(2 * n_h, 1024))
         log("  GRU rows", n_h, "L", L, "wdtype", wd)
