@@ -39,8 +39,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1950)
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=None, help="timed frames (default: all but the warm-up)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed frames (default 50; check config 5)")
     ap.add_argument("--config", default="large")
     ap.add_argument("--qmode", default=None, help="sign | sigdig1 | sigdig2 | sigdig3 | exact")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -67,6 +67,29 @@ def qmode_of(arg, cfg):
 
 def qmode_name(qm, k):
     return {0: "exact", 1: "sign", 2: "sigdig%d" % k}[qm]
+
+
+def counter_traffic(workload, stage):
+    """HBM bytes per launch of `stage` (FETCH_SIZE + WRITE_SIZE, scaled by the
+    plain-copy calibration) from the committed counter summaries under
+    profiles/, or None when none covers this workload or the kernel's sources
+    have changed since the counters were taken."""
+    import glob
+
+    from paper_1801_09866_amd.profsum import KERNELS, source_sha
+    files = next((f for st, f in KERNELS.values() if st == stage), None)
+    if files is None:
+        return None
+    sha = source_sha(files)
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_counters_*.txt"))):
+        with open(path) as fh:
+            for line in fh:
+                parts = line.split()
+                if len(parts) == 6 and parts[0] == "traffic" and parts[1] == workload and parts[2] == stage:
+                    kv = dict(x.split("=", 1) for x in parts[3:])
+                    if kv.get("source_sha256") == sha:
+                        return int(kv["fetch_bytes"]) + int(kv["write_bytes"])
+    return None
 
 
 def algorithmic_work(cfg, st, qm, frames):
@@ -119,6 +142,12 @@ def main():
     from paper_1801_09866_amd.workload import CONFIGS, make_workload
 
     cfg = CONFIGS[args.config]
+    if args.warmup is None:
+        args.warmup = 5 if cfg.queries == 0 else 50
+    if args.steps is None:
+        args.steps = cfg.frames - args.warmup
+    if cfg.queries == 0:
+        return main_check(args, cfg)
     qm, qk = qmode_of(args.qmode, cfg)
     n_frames = min(cfg.frames, args.warmup + args.steps)
     W, K = min(args.warmup, n_frames - 1), n_frames - min(args.warmup, n_frames - 1)
@@ -212,7 +241,9 @@ def main():
         dom = max(stages, key=lambda n: stages[n]["ms_total"])
         e = stages[dom]
         roofline = {"kernel": dom, "bound": e["bound"], "achieved": e["achieved"], "peak": e["peak"],
-                    "unit": e["unit"], "frac": e["frac"], "traffic": None,
+                    "unit": e["unit"], "frac": e["frac"],
+                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), dom),
+                    "algorithmic_per_launch": round(e["algorithmic"] / e["launches"]),
                     "us_per_launch": e["us_per_launch"]}
         log("stages:", json.dumps(stages))
 
@@ -282,6 +313,141 @@ def cpu_baseline(args, wl, qm, qk, sc, run, frames):
             "sample": "frames 0..%d of the same workload from empty caches (%d queries, %.1f s)"
                       % (S - 1, nq, secs),
             "gpu_value_same_sample": round(nq / gsec, 1)}
+
+
+METRIC_CHECK = "full-vocabulary log-normalisers/sec (GRU step + logsumexp over V), H=1024 V=200k; % of fp32 MFMA roofline"
+
+
+def main_check(args, cfg):
+    """Check config: each frame's histories go through the GRU step (EXACT
+    keys, no queries), then the full-vocabulary log-normaliser of every
+    resulting h' (a [n x H] . [H x V] GEMM plus logsumexp). One step is one
+    frame; the value is log-normalisers (histories) per second."""
+    import torch
+
+    from paper_1801_09866_amd import rnnlm as R
+    from paper_1801_09866_amd.workload import make_workload
+
+    qm, qk = qmode_of(args.qmode, cfg)
+    n_frames = min(cfg.frames, args.warmup + args.steps)
+    W, K = min(args.warmup, n_frames - 1), n_frames - min(args.warmup, n_frames - 1)
+    t0 = time.time()
+    wl = make_workload(args.config, n_frames=n_frames)
+    log("workload %s generated in %.1fs: %d frames" % (args.config, time.time() - t0, n_frames))
+    m = cfg.model
+    LH = m.L * m.H
+    dev = torch.device("cuda:0")
+    sc = R.Scorer(m, wl.weights, qm, qk, max_hist=cfg.max_hist, max_query=1,
+                  cap_hist=cfg.cap_hist, cap_query=cfg.cap_query, device="cuda:0")
+    pool = torch.from_numpy(wl.pool.vec).to(dev)
+    nh = np.array([f.n_hist for f in wl.frames])
+    ho = np.concatenate([[0], np.cumsum(nh)])
+    hv = pool.index_select(0, torch.from_numpy(np.concatenate([f.pool_idx for f in wl.frames])).to(dev))
+    hw = torch.from_numpy(np.concatenate([f.hist_words for f in wl.frames]).astype(np.int32)).to(dev)
+    hnew = torch.empty((int(ho[-1]), LH), dtype=torch.float32, device=dev)
+    logz = torch.empty(int(ho[-1]), dtype=torch.float32, device=dev)
+    dummy = torch.empty(1, dtype=torch.float32, device=dev)
+    del pool
+    frames, outs = [], []
+    for i in range(n_frames):
+        frames.append(R.Frame(int(nh[i]), 0, hv.data_ptr() + int(ho[i]) * LH * 4, hw.data_ptr() + int(ho[i]) * 12,
+                              None, None))
+        outs.append(R.Out(dummy.data_ptr(), hnew.data_ptr() + int(ho[i]) * LH * 4, None, None, None, None, None))
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    L = R.load()
+    ctx = sc.ctx
+    top = (m.L - 1) * m.H
+
+    def run(lo, hi):
+        for i in range(lo, hi):
+            rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[i]), ctypes.byref(outs[i]), sp)
+            if rc == 0:
+                rc = L.rnnlm_log_normalizer(ctx, ctypes.c_void_p(hnew.data_ptr() + (int(ho[i]) * LH + top) * 4),
+                                            int(nh[i]), ctypes.c_void_p(logz.data_ptr() + int(ho[i]) * 4), sp)
+            if rc:
+                raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
+
+    if m.L != 1:
+        raise SystemExit("the check config has one layer (the normaliser reads h' rows back to back)")
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start = time.perf_counter()
+    ev0.record(stream)
+    run(W, n_frames)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    gpu_ms = ev0.elapsed_time(ev1)
+    sc.stats()   # raises on a device error
+    nlog = int(ho[n_frames] - ho[W])
+    value = nlog / (gpu_ms / 1e3)
+    z = logz[int(ho[W]):int(ho[n_frames])].double().cpu().numpy()
+    log("timed %d frames: %.3f ms GPU, %.0f log-normalisers/s" % (K, gpu_ms, value))
+
+    stages, roofline = {}, None
+    if not args.no_replay:
+        sc.reset()
+        run(0, W)
+        sc.profile(R.STAGES[:4] + ("lognorm_gemm", "lognorm_combine"))
+        run(W, n_frames)
+        torch.cuda.synchronize()
+        prof = sc.profile_read()
+        sc.profile(())
+        flops = 2.0 * m.H * m.V * nlog
+        for name, (ms, launches) in prof.items():
+            e = {"ms_total": round(ms, 4), "launches": launches, "us_per_launch": round(1e3 * ms / launches, 2)}
+            if name == "lognorm_gemm":
+                ach = flops / (ms / 1e3) / 1e12
+                e.update(bound="mfma", achieved=round(ach, 2), peak=PEAK["fp32_mfma_TFs"], unit="TFLOP/s",
+                         frac=round(ach / PEAK["fp32_mfma_TFs"], 4), algorithmic=flops)
+            stages[name] = e
+        g = stages["lognorm_gemm"]
+        roofline = {"kernel": "lognorm_gemm", "bound": "mfma", "achieved": g["achieved"], "peak": g["peak"],
+                    "unit": "TFLOP/s", "frac": g["frac"],
+                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), "lognorm_gemm"),
+                    "us_per_launch": g["us_per_launch"]}
+        log("stages:", json.dumps(stages))
+
+    cpu = None
+    if not args.no_cpu:
+        from threadpoolctl import threadpool_info
+
+        from oracle import Oracle, log_normalizer
+        o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
+                   cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
+        t = time.perf_counter()
+        S = cnt = 0
+        for fr in wl.frames:
+            res = o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
+            log_normalizer(res.hnew[:, top:top + m.H], wl.weights["U_out"], wl.weights["b_out"])
+            cnt += fr.n_hist
+            S += 1
+            if time.perf_counter() - t >= args.cpu_seconds:
+                break
+        secs = time.perf_counter() - t
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        cpu = {"value": round(cnt / secs, 2), "unit": "log-normalisers/s", "cores": int(threads), "kind": "oracle",
+               "sample": "frames 0..%d of the same workload (%d histories, %.1f s)" % (S - 1, cnt, secs)}
+        log("oracle: %d frames, %d log-normalisers in %.1fs" % (S, cnt, secs))
+
+    line = {
+        "metric": METRIC_CHECK, "value": round(value, 1), "unit": "log-normalisers/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(gpu_ms / K, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "check: V=%d E=%d H=%d L=%d, %d histories/frame, EXACT keys, logsumexp over V"
+                               % (m.V, m.E, m.H, m.L, cfg.hists), "frames_timed": K},
+        "wall_ms": round(wall * 1e3, 3),
+        # NCE self-normalisation: how far log Z is from 0 over the timed histories
+        "logz": {"mean": round(float(z.mean()), 6), "sd": round(float(z.std()), 6),
+                 "min": round(float(z.min()), 6), "max": round(float(z.max()), 6)},
+        "roofline": roofline,
+        "stages": stages,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

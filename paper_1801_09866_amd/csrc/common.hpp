@@ -138,6 +138,18 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 // for divergent become exec-masked regions, and a matrix instruction inside
 // such a region still writes its accumulator when no lane is active. Every
 // branch around an MFMA must therefore depend on scalars only.
+// Load through a pointer known to address global memory. Pointers read from
+// memory or chosen by a select are generic to the compiler, which then emits
+// flat loads (they also count against the LDS wait counter); this spells out
+// the global address space.
+template <typename T>
+__device__ __forceinline__ T ldg(const void *p) {
+    static_assert(sizeof(T) == 16 || sizeof(T) == 8, "16- or 8-byte loads");
+    typedef unsigned int raw __attribute__((ext_vector_type(sizeof(T) / 4)));
+    const raw v = *reinterpret_cast<const __attribute__((address_space(1))) raw *>(reinterpret_cast<uintptr_t>(p));
+    return __builtin_bit_cast(T, v);
+}
+
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 __device__ __forceinline__ float wave_sum(float v) {

@@ -174,12 +174,12 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
             if (!src.valid) return T{0, 0, 0, 0};
             if (!BF16W) {
                 const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
-                return __builtin_bit_cast(T, *reinterpret_cast<const float4 *>(p));
+                return __builtin_bit_cast(T, ldg<float4>(p));
             }
             if (k < Kx && src.x_bf16)
-                return __builtin_bit_cast(T, *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(src.x) + k));
+                return __builtin_bit_cast(T, ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k));
             const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
-            return __builtin_bit_cast(T, pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4)));
+            return __builtin_bit_cast(T, pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4)));
         };
         auto load = [&](MdOps<BF16W> &o, int sc) {
 #pragma unroll
@@ -188,9 +188,9 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
                 if (st < s1) {
                     const int k = st * KS;
                     o.a[c] = loadA(k + kq);
-                    o.r[c] = *reinterpret_cast<const T *>(pr + k);
-                    o.z[c] = *reinterpret_cast<const T *>(pz + k);
-                    o.n[c] = *reinterpret_cast<const T *>(pn + k);
+                    o.r[c] = ldg<T>(pr + k);
+                    o.z[c] = ldg<T>(pz + k);
+                    o.n[c] = ldg<T>(pn + k);
                 }
             }
         };
@@ -296,12 +296,12 @@ __device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, f
         if (!rs.valid) return T{0, 0, 0, 0};
         if (!BF16W) {
             const float *p = k < Kx ? reinterpret_cast<const float *>(rs.x) + k : rs.h + (k - Kx);
-            return __builtin_bit_cast(T, *reinterpret_cast<const float4 *>(p));
+            return __builtin_bit_cast(T, ldg<float4>(p));
         }
         if (k < Kx && rs.x_bf16)
-            return __builtin_bit_cast(T, *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(rs.x) + k));
+            return __builtin_bit_cast(T, ldg<uint4>(reinterpret_cast<const uint16_t *>(rs.x) + k));
         const float *p = k < Kx ? reinterpret_cast<const float *>(rs.x) + k : rs.h + (k - Kx);
-        return __builtin_bit_cast(T, pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4)));
+        return __builtin_bit_cast(T, pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4)));
     };
 
     f4_t accx[N_TILES], acch[N_TILES];
@@ -314,7 +314,7 @@ __device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, f
             const int st = p0 + c;
             if (st < s1) {   // wave-uniform
                 const int k = st * KS;
-                b[c] = wcol ? *reinterpret_cast<const T *>(wrow + k) : T{0, 0, 0, 0};
+                b[c] = wcol ? ldg<T>(wrow + k) : T{0, 0, 0, 0};
 #pragma unroll
                 for (int t = 0; t < N_TILES; ++t)
                     if (t < nt) a[t][c] = loadA(src[t], k + kq);
@@ -400,10 +400,10 @@ __device__ void gru_mfma_f32(const Dev &d, const FrameArgs &f, int layer, int M,
     auto load = [&](int k0) {
         const int k = k0 + a_k;
         if (!src.valid) ra = make_float4(0.f, 0.f, 0.f, 0.f);
-        else if (k < Kx) ra = *reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(src.x) + k);
-        else ra = *reinterpret_cast<const float4 *>(src.h + (k - Kx));
-        rb0 = *reinterpret_cast<const float4 *>(bp0 + k0);
-        if (has_b1) rb1 = *reinterpret_cast<const float4 *>(bp1 + k0);
+        else if (k < Kx) ra = ldg<float4>(reinterpret_cast<const float *>(src.x) + k);
+        else ra = ldg<float4>(src.h + (k - Kx));
+        rb0 = ldg<float4>(bp0 + k0);
+        if (has_b1) rb1 = ldg<float4>(bp1 + k0);
     };
     auto store = [&](int buf) {
         *reinterpret_cast<float4 *>(&As[buf][a_row][a_k]) = ra;
@@ -491,17 +491,17 @@ __device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M
             ra = make_uint4(0, 0, 0, 0);
         } else if (k < Kx) {
             if (src.x_bf16) {
-                ra = *reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(src.x) + k);
+                ra = ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k);
             } else {
                 const float *p = reinterpret_cast<const float *>(src.x) + k;
-                ra = pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
+                ra = pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4));
             }
         } else {
             const float *p = src.h + (k - Kx);
-            ra = pack_bf16x8(*reinterpret_cast<const float4 *>(p), *reinterpret_cast<const float4 *>(p + 4));
+            ra = pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4));
         }
-        rb0 = *reinterpret_cast<const uint4 *>(bp0 + k0);
-        if (has_b1) rb1 = *reinterpret_cast<const uint4 *>(bp1 + k0);
+        rb0 = ldg<uint4>(bp0 + k0);
+        if (has_b1) rb1 = ldg<uint4>(bp1 + k0);
     };
     auto store = [&](int buf) {
         *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k]) = ra;

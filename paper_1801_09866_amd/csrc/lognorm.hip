@@ -12,7 +12,14 @@ namespace rn {
 
 typedef float f4_t __attribute__((ext_vector_type(4)));
 
-constexpr int LN_BM = 256, LN_BN = 128, LN_BK = 16, LN_LD = LN_BK + 4;
+// A block takes all n <= 256 rows and LN_NC x 16 vocabulary rows; 8 waves of
+// 32 rows each. 13 column tiles (208 rows) leave 962 vocabulary tiles at
+// V = 200,000: under two rounds over the 256 CUs, with little idle tail.
+// K advances 16 at a time through double-buffered LDS (32 at a time measured
+// slower: more registers live across the barrier).
+constexpr int LN_BM = 256, LN_NC = 13, LN_BN = 16 * LN_NC, LN_BK = 16, LN_LD = LN_BK + 4;
+static_assert(LN_BK == 16 && LN_BM == 256 && LN_BN > 128 && LN_BN <= 256,
+              "loaders: 4 threads x 4 k per row, rows tid / 4 + 128 j");
 
 int lognorm_tiles(int V) { return (V + LN_BN - 1) / LN_BN; }
 
@@ -24,66 +31,76 @@ __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int
     const int H = d.H, V = d.V;
     const float *U = reinterpret_cast<const float *>(d.U_out);
 
-    // A: 256 rows x 16 k = 1024 float4, two per thread; B: 128 x 16 = 512, one
-    const int a_r0 = tid >> 2, a_r1 = a_r0 + 128, a_k = (tid & 3) * 4;
-    const int b_r = tid >> 2, b_k = (tid & 3) * 4;
-    const bool a_ok0 = a_r0 < n, a_ok1 = a_r1 < n, b_ok = v0 + b_r < V;
-    const float *ap0 = h + (size_t)(a_ok0 ? a_r0 : 0) * H + a_k;
-    const float *ap1 = h + (size_t)(a_ok1 ? a_r1 : 0) * H + a_k;
-    const float *bp = U + (size_t)(b_ok ? v0 + b_r : 0) * H + b_k;
-    const float4 zero = make_float4(0.f, 0.f, 0.f, 0.f);
-
-    float4 ra0, ra1, rb;
-    auto load = [&](int k0) {
-        ra0 = a_ok0 ? *reinterpret_cast<const float4 *>(ap0 + k0) : zero;
-        ra1 = a_ok1 ? *reinterpret_cast<const float4 *>(ap1 + k0) : zero;
-        rb = b_ok ? *reinterpret_cast<const float4 *>(bp + k0) : zero;
+    // Rows past n (A) or past V (B) read row 0, always in bounds and finite;
+    // their products only reach output rows that are not written and logits
+    // the epilogue masks, so no select sits between a load and its use (a
+    // select right after the load would make every K step wait for memory).
+    const int lr = tid >> 2, lk = (tid & 3) * 4;
+    // A rows lr and lr + 128; B rows lr and, where the tile has it, lr + 128.
+    // Named registers: loop-carried arrays of these end up in scratch.
+    const int rb1 = lr + 128;
+    const bool b_last = rb1 < LN_BN;
+    auto arow = [&](int r) { return h + (size_t)(r < n ? r : 0) * H + lk; };
+    auto brow = [&](int r) { return U + (size_t)(r < LN_BN && v0 + r < V ? v0 + r : 0) * H + lk; };
+    const float *pa0 = arow(lr), *pa1 = arow(lr + 128);
+    const float *pb0 = brow(lr), *pb1 = brow(rb1);
+    auto ld = [](const float *p) { return *reinterpret_cast<const float4 *>(p); };
+    float4 a0 = ld(pa0), a1 = ld(pa1);
+    float4 b0 = ld(pb0), b1 = ld(pb1);
+    auto stage = [&](int buf) {
+        *reinterpret_cast<float4 *>(&As[buf][lr][lk]) = a0;
+        *reinterpret_cast<float4 *>(&As[buf][lr + 128][lk]) = a1;
+        *reinterpret_cast<float4 *>(&Bs[buf][lr][lk]) = b0;
+        if (b_last) *reinterpret_cast<float4 *>(&Bs[buf][rb1][lk]) = b1;
     };
-    auto store = [&](int buf) {
-        *reinterpret_cast<float4 *>(&As[buf][a_r0][a_k]) = ra0;
-        *reinterpret_cast<float4 *>(&As[buf][a_r1][a_k]) = ra1;
-        *reinterpret_cast<float4 *>(&Bs[buf][b_r][b_k]) = rb;
-    };
+    stage(0);
+    __syncthreads();
 
-    f4_t acc[2][8];
+    f4_t acc[2][LN_NC];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 8; ++b) acc[a][b] = f4_t{0, 0, 0, 0};
+        for (int b = 0; b < LN_NC; ++b) acc[a][b] = f4_t{0, 0, 0, 0};
 
     const int fr = lane & 15, fk = 4 * (lane >> 4);
     const int nk = H / LN_BK;
-    load(0);
-    store(0);
-    __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
-        if (kt + 1 < nk) load((kt + 1) * LN_BK);
-        float4 a[2], b[8];
+        const bool more = kt + 1 < nk;   // block-uniform
+        if (more) {   // next K slice in flight while this one multiplies
+            const int k0 = (kt + 1) * LN_BK;
+            a0 = ld(pa0 + k0);
+            a1 = ld(pa1 + k0);
+            b0 = ld(pb0 + k0);
+            b1 = ld(pb1 + k0);
+        }
 #pragma unroll
-        for (int r = 0; r < 2; ++r) a[r] = *reinterpret_cast<const float4 *>(&As[buf][w * 32 + r * 16 + fr][fk]);
+        for (int hk = 0; hk < LN_BK; hk += 16) {
+            float4 a[2];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) b[c] = *reinterpret_cast<const float4 *>(&Bs[buf][c * 16 + fr][fk]);
+            for (int r = 0; r < 2; ++r) a[r] = *reinterpret_cast<const float4 *>(&As[buf][w * 32 + r * 16 + fr][hk + fk]);
+            // one B fragment at a time: 8 MFMAs per LDS read keeps few registers live
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const float av[4] = {a[r].x, a[r].y, a[r].z, a[r].w};
+            for (int c = 0; c < LN_NC; ++c) {
+                const float4 b = *reinterpret_cast<const float4 *>(&Bs[buf][c * 16 + fr][hk + fk]);
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const float bv[4] = {b[c].x, b[c].y, b[c].z, b[c].w};
-#pragma unroll
-                for (int s = 0; s < 4; ++s)
-                    acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s], bv[s], acc[r][c], 0, 0, 0);
+                for (int r = 0; r < 2; ++r) {
+                    acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r].x, b.x, acc[r][c], 0, 0, 0);
+                    acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r].y, b.y, acc[r][c], 0, 0, 0);
+                    acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r].z, b.z, acc[r][c], 0, 0, 0);
+                    acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[r].w, b.w, acc[r][c], 0, 0, 0);
+                }
             }
         }
-        if (kt + 1 < nk) store(buf ^ 1);
+        if (more) stage(buf ^ 1);
         __syncthreads();
     }
 
     // epilogue: logits of this lane's columns, then per-row (max, sum exp)
-    float bias[8];
-    bool valid[8];
+    float bias[LN_NC];
+    bool valid[LN_NC];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
+    for (int c = 0; c < LN_NC; ++c) {
         const int v = v0 + c * 16 + fr;
         valid[c] = v < V;
         bias[c] = valid[c] ? d.b_out[v] : 0.0f;
@@ -95,13 +112,13 @@ __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int
         for (int e = 0; e < 4; ++e) {
             float m = -INFINITY;
 #pragma unroll
-            for (int c = 0; c < 8; ++c)
+            for (int c = 0; c < LN_NC; ++c)
                 if (valid[c]) m = fmaxf(m, acc[r][c][e] + bias[c]);
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
             float sum = 0.0f;
 #pragma unroll
-            for (int c = 0; c < 8; ++c)
+            for (int c = 0; c < LN_NC; ++c)
                 if (valid[c]) sum += expf(acc[r][c][e] + bias[c] - m);
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, 64);

@@ -53,8 +53,8 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
         if (!BF16) {
             const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
             for (int e = lane * 4; e < d.H; e += 256) {
-                const float4 a = *reinterpret_cast<const float4 *>(u + e);
-                const float4 b = *reinterpret_cast<const float4 *>(h + e);
+                const float4 a = ldg<float4>(u + e);
+                const float4 b = ldg<float4>(h + e);
                 acc = fmaf(a.x, b.x, acc);
                 acc = fmaf(a.y, b.y, acc);
                 acc = fmaf(a.z, b.z, acc);
@@ -63,9 +63,9 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
         } else {
             const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
             for (int e = lane * 8; e < d.H; e += 512) {
-                const uint4 a = *reinterpret_cast<const uint4 *>(u + e);
-                const float4 b0 = *reinterpret_cast<const float4 *>(h + e);
-                const float4 b1 = *reinterpret_cast<const float4 *>(h + e + 4);
+                const uint4 a = ldg<uint4>(u + e);
+                const float4 b0 = ldg<float4>(h + e);
+                const float4 b1 = ldg<float4>(h + e + 4);
                 acc = fmaf(__uint_as_float(a.x << 16), b0.x, acc);
                 acc = fmaf(__uint_as_float(a.x & 0xFFFF0000u), b0.y, acc);
                 acc = fmaf(__uint_as_float(a.y << 16), b0.z, acc);
@@ -121,7 +121,7 @@ __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f,
     if (f.hnew) {
         const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
         float4 *dst = reinterpret_cast<float4 *>(f.hnew + (size_t)i * d.LH);
-        for (int e = lane; e < d.LH / 4; e += 64) dst[e] = src[e];
+        for (int e = lane; e < d.LH / 4; e += 64) dst[e] = ldg<float4>(src + e);
     }
 }
 

@@ -1,11 +1,19 @@
 """Summarise rocprofv3 CSV output (kernel stats and per-dispatch counters).
 
     python -m paper_1801_09866_amd.profsum <rocprofv3 output dir> [--copy-bytes N]
+    python -m paper_1801_09866_amd.profsum --traffic WORKLOAD --fetch DIR --write DIR \
+        --fetch-scale B --write-scale B
 
-Prints, per kernel: calls, average duration; and for counter runs the mean
-of every collected counter per dispatch. With --copy-bytes, the counters of
-the plain copy kernel (the largest-grid elementwise copy in the run) are
-used to print a bytes-per-counter-unit scale factor.
+The first form prints, per kernel: calls, average duration; and for counter
+runs the mean of every collected counter per dispatch. With --copy-bytes, the
+counters of the plain copy kernel in the run are used to print a
+bytes-per-counter-unit scale factor.
+
+The second form prints one line per library kernel,
+    traffic WORKLOAD STAGE fetch_bytes=F write_bytes=W source_sha256=S
+with the mean FETCH_SIZE and WRITE_SIZE per dispatch scaled to bytes, and a
+hash of the sources the kernel is built from, so that a reader (bench.py) can
+tell whether the kernel has changed since the counters were taken.
 """
 import argparse
 import collections
@@ -37,11 +45,61 @@ def counters(d):
     return acc
 
 
+# library kernel -> (benchmark stage, source files it is built from)
+KERNELS = {
+    "rn::k_hist_key": ("hist_key", ["keys.hip"]),
+    "rn::k_frame_plan": ("frame_plan", ["plan.hip"]),
+    "rn::k_gru": ("gru_gemm", ["gru.hip"]),
+    "rn::k_score_finish": ("score_finish", ["score.hip"]),
+    "rn::k_lognorm_gemm": ("lognorm_gemm", ["lognorm.hip"]),
+    "rn::k_lognorm_combine": ("lognorm_combine", ["lognorm.hip"]),
+}
+SHARED = ["common.hpp", "kernels.hpp"]
+
+
+def source_sha(files):
+    import hashlib
+    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+    h = hashlib.sha256()
+    for f in files + SHARED:
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def stage_of(kernel_name):
+    base = kernel_name.split("(")[0].replace("void ", "").split("<")[0].strip()
+    return KERNELS.get(base)
+
+
+def traffic(a):
+    fetch, write = counters(a.fetch), counters(a.write)
+    for k in sorted(set(fetch) | set(write)):
+        st = stage_of(k)
+        if st is None:
+            continue
+        f = fetch.get(k, {}).get("FETCH_SIZE")
+        w = write.get(k, {}).get("WRITE_SIZE")
+        if not f or not w:
+            continue
+        fb = sum(f) / len(f) * a.fetch_scale
+        wb = sum(w) / len(w) * a.write_scale
+        print("traffic %s %s fetch_bytes=%d write_bytes=%d source_sha256=%s"
+              % (a.traffic, st[0], fb, wb, source_sha(st[1])))
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("dir")
+    ap.add_argument("dir", nargs="?")
     ap.add_argument("--copy-bytes", type=float, default=None)
+    ap.add_argument("--traffic", default=None, help="workload name for traffic lines")
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--fetch-scale", type=float, default=None)
+    ap.add_argument("--write-scale", type=float, default=None)
     a = ap.parse_args()
+    if a.traffic:
+        return traffic(a)
     ks = kernel_stats(a.dir)
     if ks:
         print("%-60s %8s %12s %12s %7s" % ("kernel", "calls", "avg_us", "total_ms", "pct"))
