@@ -63,8 +63,8 @@ enum { RNNLM_H_REP = 0, RNNLM_H_DUP = 1, RNNLM_HC_HIT = 2 };
 /* Per-query status: score computed (COMPUTED); copy of an earlier query of the
  * frame with the same key (Q_DUP); stored score returned (SCORE_HIT). */
 enum { RNNLM_Q_COMPUTED = 0, RNNLM_Q_DUP = 1, RNNLM_Q_SCORE_HIT = 2 };
-/* Sticky device error bits. */
-enum { RNNLM_DERR_WORD = 1, RNNLM_DERR_QHIST = 2, RNNLM_DERR_VALUE = 4 };
+/* Sticky device error bits (HANDLE: a null or misaligned history handle). */
+enum { RNNLM_DERR_WORD = 1, RNNLM_DERR_QHIST = 2, RNNLM_DERR_VALUE = 4, RNNLM_DERR_HANDLE = 8 };
 
 typedef struct rnnlm_t rnnlm_t;   /* opaque */
 
@@ -103,6 +103,15 @@ typedef struct {
     const int32_t *hist_words;  /* [n_hist][3]: (w-1, w-2, w-3); w-1 is the GRU input word; BOS = 0 pads */
     const int32_t *q_hist;      /* [n_query] index into this frame's histories */
     const int32_t *q_tgt;       /* [n_query] target word */
+    /* Optional history handles, for closing the decode loop without copies
+     * (a hypothesis extended in frame t has as history the h' of frame t):
+     * [n_hist] device addresses, each of one history's L*H fp32 row, for
+     * instance a row of an earlier frame's hnew output. When non-NULL,
+     * hist_vec is not read and may be NULL. Each address must be 16-byte
+     * aligned and point at L*H readable floats that are not written while
+     * the frame runs; a NULL or misaligned one sets RNNLM_DERR_HANDLE (a
+     * placeholder row is read instead). */
+    const uint64_t *hist_ptr;
 } rnnlm_frame;
 
 typedef struct {

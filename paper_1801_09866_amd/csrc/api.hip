@@ -198,8 +198,8 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.f_hstat = cv.take<int>(mh);
     d.f_hslot = cv.take<int>(mh);
     d.f_hptr = cv.take<unsigned long long>(mh);
-    d.f_rows = cv.take<int>(mh);
     d.f_roww = cv.take<int>(mh);
+    d.f_rowh = cv.take<unsigned long long>(mh);
     d.f_rowdst = cv.take<unsigned long long>(mh);
     d.f_hval = cv.take<float>(mh * LH);
     d.f_qkey = cv.take<int4>(mq);
@@ -285,14 +285,14 @@ RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm
     if (fr->n_hist < 0 || fr->n_hist > c.max_hist) return fail(RNNLM_EINVAL, "n_hist %d outside [0, %d]", fr->n_hist, c.max_hist);
     if (fr->n_query < 0 || fr->n_query > c.max_query) return fail(RNNLM_EINVAL, "n_query %d outside [0, %d]", fr->n_query, c.max_query);
     if (fr->n_query > 0 && fr->n_hist == 0) return fail(RNNLM_EINVAL, "queries without histories");
-    if (fr->n_hist > 0 && (!fr->hist_vec || !fr->hist_words)) return fail(RNNLM_EINVAL, "null history arrays");
+    if (fr->n_hist > 0 && ((!fr->hist_vec && !fr->hist_ptr) || !fr->hist_words)) return fail(RNNLM_EINVAL, "null history arrays");
     if (fr->n_query > 0 && (!fr->q_hist || !fr->q_tgt || !out->scores)) return fail(RNNLM_EINVAL, "null query arrays or scores");
     if (fr->n_hist == 0) return RNNLM_OK;
-    if (reinterpret_cast<uintptr_t>(fr->hist_vec) & 15) return fail(RNNLM_EINVAL, "hist_vec must be 16-byte aligned");
+    if (!fr->hist_ptr && (reinterpret_cast<uintptr_t>(fr->hist_vec) & 15)) return fail(RNNLM_EINVAL, "hist_vec must be 16-byte aligned");
     if (out->hnew && (reinterpret_cast<uintptr_t>(out->hnew) & 15)) return fail(RNNLM_EINVAL, "hnew must be 16-byte aligned");
     rn::FrameArgs f;
     f.n_hist = fr->n_hist; f.n_query = fr->n_query;
-    f.hist_vec = fr->hist_vec; f.hist_words = fr->hist_words; f.q_hist = fr->q_hist; f.q_tgt = fr->q_tgt;
+    f.hist_vec = fr->hist_vec; f.hist_ptr = reinterpret_cast<const rn::u64 *>(fr->hist_ptr); f.hist_words = fr->hist_words; f.q_hist = fr->q_hist; f.q_tgt = fr->q_tgt;
     f.scores = out->scores; f.hnew = out->hnew; f.q_status = out->q_status; f.h_status = out->h_status;
     f.q_rep = out->q_rep; f.h_rep = out->h_rep; f.h_hash = reinterpret_cast<rn::u64 *>(out->h_hash);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);

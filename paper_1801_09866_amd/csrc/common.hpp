@@ -31,6 +31,7 @@ constexpr int QF_PROBE = 32;   // the history key was cached before the frame: p
 struct FrameArgs {
     int n_hist, n_query;
     const float *hist_vec;
+    const u64 *hist_ptr;   // optional per-history row addresses (replace hist_vec)
     const int32_t *hist_words, *q_hist, *q_tgt;
     float *scores, *hnew;
     uint8_t *q_status, *h_status;
@@ -101,8 +102,8 @@ struct Dev {
     int *f_hcslot;    // cache slot found before the frame, or -1
     int *f_hstat, *f_hslot;
     u64 *f_hptr;      // device address of each history's h' (all layers)
-    int *f_rows;      // GRU work list: history index of row r
     int *f_roww;      // GRU input word (w-1) of row r
+    u64 *f_rowh;      // address of row r's history vector (all layers)
     u64 *f_rowdst;    // where row r writes its h'
     float *f_hval;    // [max_hist][LH] h' of rows the cache did not admit
     // per-frame query scratch
@@ -133,6 +134,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 }
 
 // butterfly sum over the 64 lanes; every lane ends with the same value
+// Address of history i's L*H vector: a row of hist_vec, or its handle. A null
+// or misaligned handle is replaced by a row of the workspace (so no access
+// leaves valid memory) and reported through *bad.
+__device__ __forceinline__ const float *hist_row(const Dev &d, const FrameArgs &f, int i, bool &bad) {
+    if (!f.hist_ptr) return f.hist_vec + (size_t)i * d.LH;
+    const u64 p = f.hist_ptr[i];
+    if (p == 0 || (p & 15)) {
+        bad = true;
+        return d.f_hval;
+    }
+    return reinterpret_cast<const float *>(p);
+}
+
 // Index of the calling wave in its block, as a scalar. The compiler cannot
 // prove threadIdx.x >> 6 uniform across a wave; branches on a value it takes
 // for divergent become exec-masked regions, and a matrix instruction inside

@@ -54,8 +54,7 @@ __device__ __forceinline__ RowSrc row_source(const Dev &d, const FrameArgs &f, i
     r.x = nullptr;
     r.h = nullptr;
     if (!r.valid) return r;
-    const int i = d.f_rows[m];
-    r.h = f.hist_vec + (size_t)i * d.LH + (size_t)layer * d.H;
+    r.h = reinterpret_cast<const float *>(d.f_rowh[m]) + (size_t)layer * d.H;
     if (layer == 0) {
         const int w = d.f_roww[m];   // loaded beside f_rows, not after it
         if (d.wdtype == RNNLM_BF16) {
@@ -79,19 +78,19 @@ __device__ __forceinline__ void gru_epilogue(const Dev &d, const FrameArgs &f, i
     const float br = b[j], bz = b[d.H + j], bn = b[2 * d.H + j];
     // every load first (the stores could alias them as far as the compiler
     // knows, which would serialise one round trip per row)
-    int mrow[4], hist[4];
+    int mrow[4];
+    const float *src[4];
     float *dst[4];
     float hprev[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         mrow[e] = m0 + rb * 16 + 4 * (lane >> 4) + e;
         const bool ok = mrow[e] < M;
-        hist[e] = ok ? d.f_rows[mrow[e]] : 0;
+        src[e] = ok ? reinterpret_cast<const float *>(d.f_rowh[mrow[e]]) : nullptr;
         dst[e] = ok ? reinterpret_cast<float *>(d.f_rowdst[mrow[e]]) : nullptr;
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-        hprev[e] = mrow[e] < M ? f.hist_vec[(size_t)hist[e] * d.LH + (size_t)layer * d.H + j] : 0.0f;
+    for (int e = 0; e < 4; ++e) hprev[e] = mrow[e] < M ? src[e][(size_t)layer * d.H + j] : 0.0f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         if (mrow[e] < M) {
@@ -282,9 +281,8 @@ __device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, f
         ebr = bb[j];
         ebz = bb[d.H + j];
         ebn = bb[2 * d.H + j];
-        const int i = d.f_rows[em];
         edst = reinterpret_cast<float *>(d.f_rowdst[em]) + (size_t)layer * d.H + j;
-        ehp = f.hist_vec[(size_t)i * d.LH + (size_t)layer * d.H + j];
+        ehp = reinterpret_cast<const float *>(d.f_rowh[em])[(size_t)layer * d.H + j];
     }
     constexpr int PASS = 12;              // steps whose operands are loaded together
     T b[PASS];

@@ -129,7 +129,8 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab 
     const int lane = threadIdx.x & 63;
     const int i = blockIdx.x * 4 + wave_id();
     if (i >= f.n_hist) return;
-    const float *x = f.hist_vec + (size_t)i * d.LH;
+    bool hbad = false;   // wave-uniform: one history per wave
+    const float *x = hist_row(d, f, i, hbad);
     const int CW = d.CW;
     u64 words[kWordsPerLane];
     bool bad = false;
@@ -178,7 +179,8 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab 
     const bool anybad = __ballot(bad) != 0ull;
 
     // words of the history record (validated, clamped)
-    unsigned err = anybad ? RNNLM_DERR_VALUE : 0u;
+    // a bad handle read a placeholder row: report the handle, not its values
+    unsigned err = hbad ? RNNLM_DERR_HANDLE : (anybad ? RNNLM_DERR_VALUE : 0u);
     int w3[3];
 #pragma unroll
     for (int c = 0; c < 3; ++c) {

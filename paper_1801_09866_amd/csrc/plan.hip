@@ -99,6 +99,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
     long long ctr_v = 0;
     if (tid < C_N) ctr_v = d.ctr[tid];
     u64 h_hash[HR];
+    const float *h_src[HR];   // each history's vector (its row, or its handle)
     int h_slot[HR], h_w1[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
@@ -106,6 +107,8 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
         h_hash[r] = d.f_hhash[i];
         h_slot[r] = d.f_hcslot[i];
         h_w1[r] = d.f_words[i * 3];
+        bool unused = false;   // the keys kernel reports bad handles
+        h_src[r] = hist_row(d, f, i, unused);
     }
     int4 qk[QR];
     int qw1[QR];
@@ -359,8 +362,8 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
             d.f_hptr[i] = (u64)hp;
             if (st == RNNLM_H_REP) {
                 const int row = s_row[i];
-                d.f_rows[row] = i;
                 d.f_roww[row] = h_w1[r];
+                d.f_rowh[row] = (u64)h_src[r];
                 d.f_rowdst[row] = (u64)hp;
             }
             if (f.h_status) f.h_status[i] = (uint8_t)st;

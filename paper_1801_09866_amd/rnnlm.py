@@ -21,7 +21,7 @@ Q_EXACT, Q_SIGN, Q_SIGDIG = 0, 1, 2
 F32, BF16 = 0, 1
 H_REP, H_DUP, HC_HIT = 0, 1, 2
 Q_COMPUTED, Q_DUP, Q_SCORE_HIT = 0, 1, 2
-DERR_WORD, DERR_QHIST, DERR_VALUE = 1, 2, 4
+DERR_WORD, DERR_QHIST, DERR_VALUE, DERR_HANDLE = 1, 2, 4, 8
 DEFAULT_SEED = 0x5EED
 
 c_i32, c_i64, c_u64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p
@@ -41,7 +41,7 @@ class Weights(ctypes.Structure):
 
 class Frame(ctypes.Structure):
     _fields_ = [("n_hist", c_i32), ("n_query", c_i32), ("hist_vec", c_vp), ("hist_words", c_vp),
-                ("q_hist", c_vp), ("q_tgt", c_vp)]
+                ("q_hist", c_vp), ("q_tgt", c_vp), ("hist_ptr", c_vp)]
 
 
 class Out(ctypes.Structure):
@@ -195,13 +195,20 @@ class Scorer:
         return o
 
     def score_frame(self, hist_vec, hist_words, q_hist, q_tgt, out=None, hnew=True, debug=True,
-                    stream=None):
-        """Score one frame; all inputs are device tensors (fp32 / int32)."""
-        n_h = int(hist_vec.shape[0]) if hist_vec is not None else 0
+                    stream=None, hist_ptr=None):
+        """Score one frame; all inputs are device tensors (fp32 / int32).
+
+        hist_ptr (optional, int64 device tensor [n_hist]): device addresses of
+        the histories' L*H rows (e.g. rows of an earlier frame's hnew), used
+        instead of hist_vec, which may then be None."""
+        if hist_ptr is not None:
+            n_h = int(hist_ptr.shape[0])
+        else:
+            n_h = int(hist_vec.shape[0]) if hist_vec is not None else 0
         n_q = int(q_hist.shape[0]) if q_hist is not None else 0
         if out is None:
             out = self.alloc_out(n_h, n_q, hnew, debug)
-        fr = Frame(n_h, n_q, _ptr(hist_vec), _ptr(hist_words), _ptr(q_hist), _ptr(q_tgt))
+        fr = Frame(n_h, n_q, _ptr(hist_vec), _ptr(hist_words), _ptr(q_hist), _ptr(q_tgt), _ptr(hist_ptr))
         co = Out(*[_ptr(out.get(k)) for k in ("scores", "hnew", "q_status", "q_rep",
                                                "h_status", "h_rep", "h_hash")])
         _check(load().rnnlm_score_frame(self.ctx, ctypes.byref(fr), ctypes.byref(co), _stream(stream)))

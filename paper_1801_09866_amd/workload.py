@@ -331,3 +331,69 @@ def make_workload(name: str, n_frames=None, pool_size=None, model=None,
     frames = make_frames(cfg, pool, zipf, rframes, n_frames)
     w = make_weights(m, cfg.seed_index) if with_weights else None
     return Workload(cfg, w, pool, frames)
+
+
+# --------------------------------------------------------------------------
+# decode-loop plans: frames whose histories are the previous frames' outputs
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class DecodeFrame:
+    """One frame of a decode loop over a beam of hypotheses.
+
+    Hypothesis j of this frame has words (w-1, w-2, w-3) = words[j] and
+    queries its `fanout` candidate next words cand[j]. Its history vector is,
+    for frame 0, row j of the initial histories; later, if advanced[j], the
+    GRU output (h') of hypothesis prev[j] of the previous frame, else the same
+    history vector as hypothesis prev[j] of the previous frame (a hypothesis
+    that stays, whose queries repeat, as between word ends in a decoder).
+    """
+    words: np.ndarray      # [B, 3] int32
+    cand: np.ndarray       # [B, F] int32
+    prev: np.ndarray       # [B] int64 index into the previous frame (-1 in frame 0)
+    advanced: np.ndarray   # [B] bool
+
+    @property
+    def q_hist(self):
+        return np.repeat(np.arange(len(self.words), dtype=np.int32), self.cand.shape[1])
+
+    @property
+    def q_tgt(self):
+        return self.cand.reshape(-1).astype(np.int32)
+
+
+def decode_plan(V, beam, fanout, n_frames, stay, zipf_s, seed, init_words, shared=0):
+    """Seeded beam evolution, independent of any score: each frame keeps
+    round(stay * beam) hypotheses (chosen uniformly) and fills the rest of
+    the beam with distinct (hypothesis, candidate slot) extensions (chosen
+    uniformly); new hypotheses draw fresh Zipf candidates. init_words [beam, 3]
+    are the words of the initial histories.
+
+    shared > 0 models hypotheses that compete for the same stretch of speech:
+    each frame draws `shared` Zipf words and every new hypothesis takes its
+    candidates from them, so paths that differ only in their older words
+    re-merge on the same recent words, as in a decoding lattice."""
+    rng = np.random.default_rng(seed)
+    zipf = Zipf(V, zipf_s)
+
+    def draw_cand(n):
+        if shared <= 0:
+            return zipf.draw(rng, n * fanout).reshape(n, fanout)
+        pool = zipf.draw(rng, shared)
+        return np.stack([rng.choice(pool, fanout, replace=False) for _ in range(n)]).astype(np.int32)
+
+    words = np.asarray(init_words, dtype=np.int32).copy()
+    cand = draw_cand(beam)
+    frames = [DecodeFrame(words, cand, np.full(beam, -1, np.int64), np.zeros(beam, bool))]
+    n_keep = int(round(stay * beam))
+    for _ in range(1, n_frames):
+        keep = np.sort(rng.choice(beam, n_keep, replace=False))
+        ext = np.sort(rng.choice(beam * fanout, beam - n_keep, replace=False))
+        par, slot = ext // fanout, ext % fanout
+        w_new = np.stack([cand[par, slot], words[par, 0], words[par, 1]], axis=1).astype(np.int32)
+        c_new = draw_cand(len(par))
+        words = np.concatenate([words[keep], w_new])
+        cand = np.concatenate([cand[keep], c_new])
+        prev = np.concatenate([keep, par]).astype(np.int64)
+        adv = np.concatenate([np.zeros(n_keep, bool), np.ones(len(par), bool)])
+        frames.append(DecodeFrame(words, cand, prev, adv))
+    return frames

@@ -50,3 +50,28 @@ def test_all_configs_are_well_formed():
         assert m.H % 64 == 0 and m.E % 64 == 0
         assert 1 <= m.L <= 2 and 1 <= m.maxent_order <= 4
         assert c.max_hist >= c.hists
+
+
+def test_decode_plan_is_seeded_and_well_formed():
+    from paper_1801_09866_amd.workload import decode_plan
+    init = np.arange(30, dtype=np.int32).reshape(10, 3) + 1
+    a = decode_plan(500, 10, 4, 6, 0.6, 1.0, 9, init)
+    b = decode_plan(500, 10, 4, 6, 0.6, 1.0, 9, init)
+    assert len(a) == 6
+    for fa, fb in zip(a, b):
+        for key in ("words", "cand", "prev", "advanced"):
+            assert np.array_equal(getattr(fa, key), getattr(fb, key))
+    assert np.array_equal(a[0].words, init) and np.all(a[0].prev == -1)
+    for t in range(1, 6):
+        f, p = a[t], a[t - 1]
+        assert f.words.shape == (10, 3) and f.cand.shape == (10, 4)
+        assert f.advanced.sum() == 4 and np.all((0 <= f.prev) & (f.prev < 10))
+        for j in range(10):
+            i = f.prev[j]
+            if f.advanced[j]:   # extended by one of its parent's candidates, words shifted
+                assert f.words[j, 0] in p.cand[i] and f.words[j, 1] == p.words[i, 0] and f.words[j, 2] == p.words[i, 1]
+            else:               # stays: same words and candidates, so its queries repeat
+                assert np.array_equal(f.words[j], p.words[i]) and np.array_equal(f.cand[j], p.cand[i])
+        ext = {(int(f.prev[j]), int(f.words[j, 0])) for j in range(10) if f.advanced[j]}
+        assert len(ext) == 4   # distinct extensions
+    assert np.array_equal(a[1].q_hist, np.repeat(np.arange(10), 4))
