@@ -47,6 +47,8 @@ def parse():
                     help="time budget of the oracle sample (whole frames from frame 0)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the cpu_baseline leg")
     ap.add_argument("--no-replay", action="store_true", help="skip the per-stage timing replay")
+    ap.add_argument("--maxent", action="store_true",
+                    help="check config: normalise the full output (NCE + MaxEnt logits of every word)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -363,8 +365,13 @@ def main_check(args, cfg):
         for i in range(lo, hi):
             rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[i]), ctypes.byref(outs[i]), sp)
             if rc == 0:
-                rc = L.rnnlm_log_normalizer(ctx, ctypes.c_void_p(hnew.data_ptr() + (int(ho[i]) * LH + top) * 4),
-                                            int(nh[i]), ctypes.c_void_p(logz.data_ptr() + int(ho[i]) * 4), sp)
+                hp = ctypes.c_void_p(hnew.data_ptr() + (int(ho[i]) * LH + top) * 4)
+                zp = ctypes.c_void_p(logz.data_ptr() + int(ho[i]) * 4)
+                if args.maxent:   # the context of the next word after each h' is its history's words
+                    rc = L.rnnlm_log_normalizer_maxent(ctx, hp, ctypes.c_void_p(hw.data_ptr() + int(ho[i]) * 12),
+                                                       int(nh[i]), zp, sp)
+                else:
+                    rc = L.rnnlm_log_normalizer(ctx, hp, int(nh[i]), zp, sp)
             if rc:
                 raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
 
@@ -415,14 +422,18 @@ def main_check(args, cfg):
     if not args.no_cpu:
         from threadpoolctl import threadpool_info
 
-        from oracle import Oracle, log_normalizer
+        from oracle import Oracle, log_normalizer, log_normalizer_maxent
         o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
                    cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
         t = time.perf_counter()
         S = cnt = 0
         for fr in wl.frames:
             res = o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
-            log_normalizer(res.hnew[:, top:top + m.H], wl.weights["U_out"], wl.weights["b_out"])
+            if args.maxent:
+                log_normalizer_maxent(res.hnew[:, top:top + m.H], wl.weights["U_out"], wl.weights["b_out"],
+                                      wl.weights["maxent"], fr.hist_words, m.maxent_order, m.maxent_log2)
+            else:
+                log_normalizer(res.hnew[:, top:top + m.H], wl.weights["U_out"], wl.weights["b_out"])
             cnt += fr.n_hist
             S += 1
             if time.perf_counter() - t >= args.cpu_seconds:
@@ -437,8 +448,10 @@ def main_check(args, cfg):
         "metric": METRIC_CHECK, "value": round(value, 1), "unit": "log-normalisers/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(gpu_ms / K, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": "check: V=%d E=%d H=%d L=%d, %d histories/frame, EXACT keys, logsumexp over V"
-                               % (m.V, m.E, m.H, m.L, cfg.hists), "frames_timed": K},
+        "config": {"workload": "check: V=%d E=%d H=%d L=%d, %d histories/frame, EXACT keys, logsumexp over V%s"
+                               % (m.V, m.E, m.H, m.L, cfg.hists,
+                                  " of NCE + MaxEnt (orders 2..%d) logits" % m.maxent_order if args.maxent else ""),
+                   "frames_timed": K, "maxent": bool(args.maxent)},
         "wall_ms": round(wall * 1e3, 3),
         # NCE self-normalisation: how far log Z is from 0 over the timed histories
         "logz": {"mean": round(float(z.mean()), 6), "sd": round(float(z.std()), 6),

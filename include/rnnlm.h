@@ -158,6 +158,18 @@ int rnnlm_cache_reset(rnnlm_t *ctx, void *stream);
  * h_top: [n][H] fp32 device; logz: [n] fp32 device; n <= max_hist. */
 int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *logz, void *stream);
 
+/* The same normaliser over the full model output: every word's logit also
+ * gets its hashed n-gram MaxEnt weights (Sec. 2.3) after history i's context,
+ *   logz[i] = log sum_v exp(U_out[v] . h_top[i] + b_out[v]
+ *                           + sum_{o=2..N} maxent[slot_o(words[i], v)]),
+ * with the slots the scores use. words: [n][3] int32 device, (w-1, w-2, w-3)
+ * of each history (the word of the GRU step that made h_top[i] is w-1 of the
+ * next step, so pass the context of the queries to be normalised). A word
+ * outside [0, V) sets RNNLM_DERR_WORD and is read as 0. Other arguments and
+ * errors as rnnlm_log_normalizer. */
+int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, const int32_t *words, int32_t n, float *logz,
+                                void *stream);
+
 /* Copy the device statistics into *stats (host memory); synchronises `stream`.
  * Returns RNNLM_EDEVICE if the sticky device flag is set. */
 int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *stats, void *stream);

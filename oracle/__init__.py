@@ -16,5 +16,5 @@ from .rnnlm_oracle import (  # noqa: F401
     Q_EXACT, Q_SIGN, Q_SIGDIG,
     H_REP, H_DUP, HC_HIT, Q_COMPUTED, Q_DUP, Q_SCORE_HIT,
     mix64, hist_key_hash, maxent_index, quantize, dequantize, code_words,
-    gru_step, nce_score, log_normalizer, Oracle, FrameResult,
+    gru_step, nce_score, log_normalizer, log_normalizer_maxent, Oracle, FrameResult,
 )

@@ -262,6 +262,30 @@ def log_normalizer(h_top, U_out, b_out, chunk=8192):
     return m + np.log(np.sum(np.exp(a - m[:, None]), axis=1))
 
 
+def log_normalizer_maxent(h_top, U_out, b_out, maxent, words, max_order, log2, chunk=8192):
+    """logZ_i over the full model output: every word v's logit is the NCE
+    logit plus its hashed n-gram MaxEnt weights after history i's context
+    words (Sec. 2.2 with the Sec. 2.3 bypass), orders 2..max_order, the same
+    slots the scores use (maxent_index). words: [n, 3] (w-1, w-2, w-3)."""
+    h = np.asarray(h_top, dtype=np.float64)
+    words = np.asarray(words, dtype=np.int64)
+    V = U_out.shape[0]
+    if words.shape != (h.shape[0], 3) or words.min(initial=0) < 0 or words.max(initial=0) >= V:
+        raise ValueError("words must be [n, 3] ids in [0, V)")
+    a = np.empty((h.shape[0], V), dtype=np.float64)
+    for v0 in range(0, V, chunk):
+        u = np.asarray(U_out[v0:v0 + chunk], dtype=np.float64)
+        a[:, v0:v0 + chunk] = h @ u.T + np.asarray(b_out[v0:v0 + chunk], np.float64)
+    lam = np.asarray(maxent, dtype=np.float64)
+    v = np.arange(V, dtype=np.int64)
+    for i in range(h.shape[0]):
+        for o in range(2, max_order + 1):
+            ctx = [np.full(V, words[i, c], dtype=np.int64) for c in range(o - 1)]
+            a[i] += lam[maxent_index(o, ctx, v, log2)]
+    m = a.max(axis=1)
+    return m + np.log(np.sum(np.exp(a - m[:, None]), axis=1))
+
+
 # --------------------------------------------------------------------------
 # frame-wise scoring with the two caches
 # --------------------------------------------------------------------------

@@ -323,7 +323,8 @@ RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
     return RNNLM_OK;
 }
 
-RNNLM_API int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *logz, void *stream) {
+static int log_normalizer(rnnlm_t *ctx, const float *h_top, const int32_t *words, int32_t n, float *logz,
+                          void *stream, const char *name) {
     if (!ctx) return fail(RNNLM_EINVAL, "null context");
     if (n < 0 || n > ctx->cfg.max_hist) return fail(RNNLM_EINVAL, "n %d outside [0, %d]", n, ctx->cfg.max_hist);
     if (n == 0) return RNNLM_OK;
@@ -334,12 +335,22 @@ RNNLM_API int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, 
     for (int r0 = 0; r0 < n; r0 += 256) {
         const int nr = n - r0 < 256 ? n - r0 : 256;
         const float *hb = h_top + (size_t)r0 * ctx->cfg.H;
-        rn::launch_lognorm_gemm(ctx->dev, hb, nr, s, StageTimer(ctx, 8).ts);
+        rn::launch_lognorm_gemm(ctx->dev, hb, words ? words + (size_t)r0 * 3 : nullptr, nr, s, StageTimer(ctx, 8).ts);
         rn::launch_lognorm_combine(ctx->dev, nr, logz + r0, s, StageTimer(ctx, 9).ts);
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "rnnlm_log_normalizer launch");
+    if (e != hipSuccess) return hip_fail(e, name);
     return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *logz, void *stream) {
+    return log_normalizer(ctx, h_top, nullptr, n, logz, stream, "rnnlm_log_normalizer launch");
+}
+
+RNNLM_API int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, const int32_t *words, int32_t n,
+                                          float *logz, void *stream) {
+    if (n > 0 && !words) return fail(RNNLM_EINVAL, "null words");
+    return log_normalizer(ctx, h_top, words, n, logz, stream, "rnnlm_log_normalizer_maxent launch");
 }
 
 RNNLM_API int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *st, void *stream) {

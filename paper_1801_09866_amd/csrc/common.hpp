@@ -232,12 +232,19 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h) {
 }
 
 // slot of the order-n MaxEnt n-gram (w-1 .. w-(n-1), target) in a 2^log2 table
-__device__ __forceinline__ uint32_t maxent_slot(int order, int w1, int w2, int w3, int tgt, int log2) {
+// order-n MaxEnt feature: the order seeds a fold of the n-1 context words
+// (most recent first), then the target; the prefix (everything before the
+// target) is shared by all targets after the same context
+__device__ __forceinline__ u64 maxent_prefix(int order, int w1, int w2, int w3) {
     u64 g = mix64((u64)order * kPhi);
     g = mix64(g ^ (u64)(w1 + 1));
     if (order >= 3) g = mix64(g ^ (u64)(w2 + 1));
     if (order >= 4) g = mix64(g ^ (u64)(w3 + 1));
-    g = mix64(g ^ (u64)(tgt + 1));
+    return g;
+}
+
+__device__ __forceinline__ uint32_t maxent_slot(int order, int w1, int w2, int w3, int tgt, int log2) {
+    const u64 g = mix64(maxent_prefix(order, w1, w2, w3) ^ (u64)(tgt + 1));
     return (uint32_t)(g & ((1ull << log2) - 1));
 }
 

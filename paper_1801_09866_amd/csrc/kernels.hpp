@@ -39,7 +39,9 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
 
 
 int lognorm_tiles(int V);
-void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s, Stamp ts = {});
+// words: optional [n][3] context words; when given, the MaxEnt weights of
+// every vocabulary word after each row's context join its logit
+void launch_lognorm_gemm(const Dev &d, const float *h, const int32_t *words, int n, hipStream_t s, Stamp ts = {});
 void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s, Stamp ts = {});
 
 }  // namespace rn

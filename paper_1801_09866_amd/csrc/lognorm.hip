@@ -1,6 +1,8 @@
 // Full-vocabulary log normaliser (Sec. 2.2: the normalisation over V that
 // NCE lets the decoder skip), used to measure NCE self-normalisation:
-//   logZ_i = log sum_v exp(U_out[v] . h_i + b_out[v]).
+//   logZ_i = log sum_v exp(U_out[v] . h_i + b_out[v] [+ MaxEnt_i(v)]),
+// where the optional MaxEnt term (Sec. 2.3) adds, for every word v, the
+// hashed n-gram weights of v after history i's context words.
 // Pass 1: an fp32 MFMA GEMM over vocabulary tiles; each block keeps all n <=
 // 256 rows of h and 128 vocabulary rows, and its epilogue reduces its logits
 // to a (max, sum exp(. - max)) pair per row. No logit reaches HBM.
@@ -23,9 +25,10 @@ static_assert(LN_BK == 16 && LN_BM == 256 && LN_BN > 128 && LN_BN <= 256,
 
 int lognorm_tiles(int V) { return (V + LN_BN - 1) / LN_BN; }
 
-__global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int n) {
+__global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, const int32_t *words, int n) {
     __shared__ float As[2][LN_BM][LN_LD];
     __shared__ float Bs[2][LN_BN][LN_LD];
+    __shared__ u64 s_g[LN_BM][3];   // MaxEnt: per row and order 2..4, the hash of its context words
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int tile = blockIdx.x, v0 = tile * LN_BN;
     const int H = d.H, V = d.V;
@@ -53,6 +56,17 @@ __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int
         *reinterpret_cast<float4 *>(&Bs[buf][lr][lk]) = b0;
         if (b_last) *reinterpret_cast<float4 *>(&Bs[buf][rb1][lk]) = b1;
     };
+    if (words && tid < LN_BM) {   // while the first K slice is in flight
+        int wv[3];
+        unsigned err = 0;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            wv[c] = tid < n ? words[tid * 3 + c] : 0;
+            if (wv[c] < 0 || wv[c] >= V) { err = RNNLM_DERR_WORD; wv[c] = 0; }
+        }
+        for (int o = 2; o <= d.me_order; ++o) s_g[tid][o - 2] = maxent_prefix(o, wv[0], wv[1], wv[2]);
+        if (err && tile == 0) atomicOr(d.derr, err);
+    }
     stage(0);
     __syncthreads();
 
@@ -106,23 +120,40 @@ __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, int
         bias[c] = valid[c] ? d.b_out[v] : 0.0f;
     }
     const int NT = gridDim.x;
+    const uint64_t me_mask = (1ull << d.me_log2) - 1;
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
+            const int row = w * 32 + r * 16 + 4 * (lane >> 4) + e;
+            float lg[LN_NC];
+#pragma unroll
+            for (int c = 0; c < LN_NC; ++c) lg[c] = acc[r][c][e] + bias[c];
+            if (words) {   // this row's n-gram weights of every column word, gathered together
+                for (int o = 2; o <= d.me_order; ++o) {
+                    const u64 g = s_g[row][o - 2];
+                    float me[LN_NC];
+#pragma unroll
+                    for (int c = 0; c < LN_NC; ++c) {
+                        const int v = v0 + c * 16 + fr;
+                        me[c] = d.maxent[mix64(g ^ (u64)(valid[c] ? v + 1 : 1)) & me_mask];
+                    }
+#pragma unroll
+                    for (int c = 0; c < LN_NC; ++c) lg[c] += me[c];
+                }
+            }
             float m = -INFINITY;
 #pragma unroll
             for (int c = 0; c < LN_NC; ++c)
-                if (valid[c]) m = fmaxf(m, acc[r][c][e] + bias[c]);
+                if (valid[c]) m = fmaxf(m, lg[c]);
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
             float sum = 0.0f;
 #pragma unroll
             for (int c = 0; c < LN_NC; ++c)
-                if (valid[c]) sum += expf(acc[r][c][e] + bias[c] - m);
+                if (valid[c]) sum += expf(lg[c] - m);
 #pragma unroll
             for (int o = 1; o < 16; o <<= 1) sum += __shfl_xor(sum, o, 64);
-            const int row = w * 32 + r * 16 + 4 * (lane >> 4) + e;
             if (fr == 0 && row < n) d.ln_part[(size_t)row * NT + tile] = make_float2(m, sum);
         }
     }
@@ -148,8 +179,8 @@ __global__ __launch_bounds__(256) void k_lognorm_combine(Dev d, int NT, float *l
     if (tid == 0) logz[row] = s[0].x + logf(s[0].y);
 }
 
-void launch_lognorm_gemm(const Dev &d, const float *h, int n, hipStream_t s, Stamp ts) {
-    launch_k(k_lognorm_gemm, lognorm_tiles(d.V), 512, s, ts, d, h, n);
+void launch_lognorm_gemm(const Dev &d, const float *h, const int32_t *words, int n, hipStream_t s, Stamp ts) {
+    launch_k(k_lognorm_gemm, lognorm_tiles(d.V), 512, s, ts, d, h, words, n);
 }
 
 void launch_lognorm_combine(const Dev &d, int n, float *logz, hipStream_t s, Stamp ts) {

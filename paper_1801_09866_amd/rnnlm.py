@@ -60,7 +60,7 @@ class Stats(ctypes.Structure):
 
 
 EXPORTS = ("rnnlm_workspace_size", "rnnlm_create", "rnnlm_score_frame", "rnnlm_cache_reset",
-           "rnnlm_log_normalizer", "rnnlm_get_stats", "rnnlm_debug_quantize", "rnnlm_profile",
+           "rnnlm_log_normalizer", "rnnlm_log_normalizer_maxent", "rnnlm_get_stats", "rnnlm_debug_quantize", "rnnlm_profile",
            "rnnlm_profile_read", "rnnlm_destroy", "rnnlm_last_error")
 NSTAGES = 10
 STAGES = ("hist_key", "frame_plan", "gru_gemm", "score_finish", "unused4", "unused5",
@@ -83,6 +83,7 @@ def load(path=LIB_PATH):
     L.rnnlm_score_frame.argtypes = [c_vp, P(Frame), P(Out), c_vp]
     L.rnnlm_cache_reset.argtypes = [c_vp, c_vp]
     L.rnnlm_log_normalizer.argtypes = [c_vp, c_vp, c_i32, c_vp, c_vp]
+    L.rnnlm_log_normalizer_maxent.argtypes = [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]
     L.rnnlm_get_stats.argtypes = [c_vp, P(Stats), c_vp]
     L.rnnlm_debug_quantize.argtypes = [c_i32, c_i32, c_vp, c_i64, c_vp, c_vp, c_vp]
     L.rnnlm_profile.argtypes = [c_vp, ctypes.c_uint32]
@@ -233,6 +234,16 @@ class Scorer:
         if out is None:
             out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
         _check(load().rnnlm_log_normalizer(self.ctx, _ptr(h_top), n, _ptr(out), _stream(stream)))
+        return out[:n]
+
+    def log_normalizer_maxent(self, h_top, words, out=None, stream=None):
+        """Normaliser over the full output: NCE logit plus each word's MaxEnt
+        weights after the row's context words ([n, 3] int32 device tensor)."""
+        n = int(h_top.shape[0])
+        if out is None:
+            out = torch.empty(max(n, 1), dtype=torch.float32, device=self.device)
+        _check(load().rnnlm_log_normalizer_maxent(self.ctx, _ptr(h_top), _ptr(words), n, _ptr(out),
+                                                  _stream(stream)))
         return out[:n]
 
     def profile(self, stages=()):

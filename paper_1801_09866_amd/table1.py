@@ -1,7 +1,8 @@
 """Synthetic redundancy sweep in the shape of the paper's Table 1.
 
     python -m paper_1801_09866_amd.table1 [--config large] [--beam 512]
-        [--fanout 4] [--frames 200] [--stay 0.5] [--shared 12] [--seed 1]
+        [--fanout 4] [--frames 200] [--stay 0.5] [--shared 12] [--focus 0.8]
+        [--wx 0.5] [--wh 0.01] [--bz -2] [--seed 1]
 
 Runs one seeded decode loop (workload.decode_plan: a beam whose hypotheses
 either stay, repeating their queries, or advance by one of their candidate
@@ -12,9 +13,19 @@ mode, the unique LM queries (scores computed), unique GRU rows, the cache
 hit ratios, the reduction against exact, and how far the scores move from
 the exact run's on the same queries; ends with one JSON line.
 
-The absolute counts depend on the synthetic model and beam dynamics (random
-weights, a seeded beam): only the shape of Table 1 (how much each
-compression merges) is comparable, not its numbers.
+History compression only merges states that have come close, which a
+trained language model's do once paths share their recent words (it
+forgets). The random-weight model of the workload configs hardly forgets, so
+the sweep rescales it into a forgetful one: input weights of scale --wx,
+recurrent weights of scale --wh, and --bz added to the update-gate bias (a
+small update gate: the new state follows the new word). The decode plan
+shares each frame's candidate words across the beam and sends a fraction
+--focus of the extensions through the frame's spoken word, so paths that
+differ in older words continue on the same recent words.
+
+The absolute counts depend on that synthetic model and beam: only the shape
+of Table 1 (how much each compression merges, and in which order) is
+comparable, not its numbers.
 """
 from __future__ import annotations
 
@@ -37,6 +48,10 @@ def main(argv=None):
     ap.add_argument("--stay", type=float, default=0.5)
     ap.add_argument("--shared", type=int, default=12,
                     help="candidate words shared by the whole beam in a frame (0: independent draws)")
+    ap.add_argument("--focus", type=float, default=0.8)
+    ap.add_argument("--wx", type=float, default=0.5, help="input-weight scale of the swept model")
+    ap.add_argument("--wh", type=float, default=0.01, help="recurrent-weight scale of the swept model")
+    ap.add_argument("--bz", type=float, default=-2.0, help="added to the update-gate bias")
     ap.add_argument("--seed", type=int, default=1)
     a = ap.parse_args(argv)
     import torch
@@ -51,13 +66,20 @@ def main(argv=None):
     rng = np.random.default_rng(a.seed)
     pick = rng.choice(len(wl.pool.vec), a.beam, replace=False)
     plan = decode_plan(m.V, a.beam, a.fanout, a.frames, a.stay, cfg.zipf_s, a.seed, wl.pool.words[pick],
-                       shared=a.shared)
+                       shared=a.shared, focus=a.focus)
+    w = dict(wl.weights)   # the workload weights use scale 0.05
+    w["W_ih"] = [(x * (a.wx / 0.05)).astype(np.float32) for x in w["W_ih"]]
+    w["W_hh"] = [(x * (a.wh / 0.05)).astype(np.float32) for x in w["W_hh"]]
+    b = [x.copy() for x in w["b_ih"]]
+    for x in b:
+        x[m.H:2 * m.H] += np.float32(a.bz)   # gate order r, z, n
+    w["b_ih"] = b
     dev = torch.device("cuda:0")
     init = torch.from_numpy(np.ascontiguousarray(wl.pool.vec[pick])).to(dev)
     nq = a.beam * a.fanout
     rows, ref = [], None
     for name, qm, qk in MODES:
-        sc = R.Scorer(m, wl.weights, qm, qk, max_hist=a.beam, max_query=nq,
+        sc = R.Scorer(m, w, qm, qk, max_hist=a.beam, max_query=nq,
                       cap_hist=a.beam * a.frames + 1, cap_query=nq * a.frames + 1)
         loop = DeviceDecodeLoop(sc, init)
         torch.cuda.synchronize()
@@ -87,7 +109,8 @@ def main(argv=None):
             r["mode"], r["queries"], r["unique_queries"], 100 * r["reduction_vs_exact"], r["unique_gru_rows"],
             r["score_hit_ratio"], r["hist_hit_ratio"], r["score_dev_mean"], r["score_dev_max"]), file=sys.stderr)
     print(json.dumps({"config": a.config, "beam": a.beam, "fanout": a.fanout, "frames": a.frames,
-                      "stay": a.stay, "shared": a.shared, "seed": a.seed, "rows": rows}))
+                      "stay": a.stay, "shared": a.shared, "focus": a.focus, "wx": a.wx, "wh": a.wh,
+                      "bz": a.bz, "seed": a.seed, "rows": rows}))
 
 
 if __name__ == "__main__":

@@ -361,7 +361,7 @@ class DecodeFrame:
         return self.cand.reshape(-1).astype(np.int32)
 
 
-def decode_plan(V, beam, fanout, n_frames, stay, zipf_s, seed, init_words, shared=0):
+def decode_plan(V, beam, fanout, n_frames, stay, zipf_s, seed, init_words, shared=0, focus=0.0):
     """Seeded beam evolution, independent of any score: each frame keeps
     round(stay * beam) hypotheses (chosen uniformly) and fills the rest of
     the beam with distinct (hypothesis, candidate slot) extensions (chosen
@@ -370,16 +370,25 @@ def decode_plan(V, beam, fanout, n_frames, stay, zipf_s, seed, init_words, share
 
     shared > 0 models hypotheses that compete for the same stretch of speech:
     each frame draws `shared` Zipf words and every new hypothesis takes its
-    candidates from them, so paths that differ only in their older words
-    re-merge on the same recent words, as in a decoding lattice."""
+    candidates from them. The first of them is the frame's spoken word: it
+    is every new hypothesis' first candidate, and a fraction `focus` of the
+    frame's extensions take it (from distinct parents). Paths that differ
+    only in older words then continue on the same recent words, as in a
+    decoding lattice."""
     rng = np.random.default_rng(seed)
     zipf = Zipf(V, zipf_s)
+    spoken = [None]
 
     def draw_cand(n):
         if shared <= 0:
             return zipf.draw(rng, n * fanout).reshape(n, fanout)
-        pool = zipf.draw(rng, shared)
-        return np.stack([rng.choice(pool, fanout, replace=False) for _ in range(n)]).astype(np.int32)
+        pool = np.unique(zipf.draw(rng, shared))
+        while len(pool) < fanout:
+            pool = np.unique(np.concatenate([pool, zipf.draw(rng, shared)]))
+        spoken[0] = int(pool[rng.integers(len(pool))])
+        rest = pool[pool != spoken[0]]
+        return np.stack([np.concatenate([[spoken[0]], rng.choice(rest, fanout - 1, replace=False)])
+                         for _ in range(n)]).astype(np.int32)
 
     words = np.asarray(init_words, dtype=np.int32).copy()
     cand = draw_cand(beam)
@@ -387,7 +396,19 @@ def decode_plan(V, beam, fanout, n_frames, stay, zipf_s, seed, init_words, share
     n_keep = int(round(stay * beam))
     for _ in range(1, n_frames):
         keep = np.sort(rng.choice(beam, n_keep, replace=False))
-        ext = np.sort(rng.choice(beam * fanout, beam - n_keep, replace=False))
+        n_adv = beam - n_keep
+        n_foc = int(round(focus * n_adv)) if shared > 0 else 0
+        if n_foc:
+            # extensions by the spoken word: distinct parents whose candidates hold it
+            holders = np.nonzero((cand == spoken[0]).any(axis=1))[0]
+            n_foc = min(n_foc, len(holders))
+            fpar = np.sort(rng.choice(holders, n_foc, replace=False))
+            fslot = np.array([int(np.nonzero(cand[i] == spoken[0])[0][0]) for i in fpar], dtype=np.int64)
+            taken = set((fpar * fanout + fslot).tolist())
+            free = np.array([e for e in range(beam * fanout) if e not in taken])
+            ext = np.sort(np.concatenate([fpar * fanout + fslot, rng.choice(free, n_adv - n_foc, replace=False)]))
+        else:
+            ext = np.sort(rng.choice(beam * fanout, n_adv, replace=False))
         par, slot = ext // fanout, ext % fanout
         w_new = np.stack([cand[par, slot], words[par, 0], words[par, 1]], axis=1).astype(np.int32)
         c_new = draw_cand(len(par))

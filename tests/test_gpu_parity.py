@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from harness import ATOL, RTOL, close, device_frame, log, make_pair, run_frames
-from oracle import Q_EXACT, Q_SIGDIG, Q_SIGN, log_normalizer
+from oracle import Q_EXACT, Q_SIGDIG, Q_SIGN, log_normalizer, log_normalizer_maxent
 from paper_1801_09866_amd import rnnlm as R
 from paper_1801_09866_amd.workload import CONFIGS, ModelCfg
 
@@ -85,3 +85,46 @@ def test_normaliser_closed_form_and_ragged_rows():
     z = sc2.log_normalizer(torch.from_numpy(h).cuda()).cpu().numpy()
     ok, err = close(z, log_normalizer(h, w2["U_out"], w2["b_out"]), ATOL, RTOL)
     assert ok, err
+
+
+def test_maxent_normaliser_against_the_oracle():
+    """Normaliser over the full output (NCE + MaxEnt for every word): ragged
+    vocabulary tail, > 256 rows, orders 2..4; zero MaxEnt weights give the
+    plain normaliser's bits; a word outside [0, V) is a sticky device error."""
+    m = ModelCfg(V=3000 + 29, E=64, H=128, L=1, wdtype=R.F32, maxent_log2=12, maxent_order=4)
+    rng = np.random.default_rng(12)
+    w = {"emb": np.zeros((m.V, m.E), np.float32), "W_ih": [np.zeros((384, 64), np.float32)],
+         "W_hh": [np.zeros((384, 128), np.float32)], "b_ih": [np.zeros(384, np.float32)],
+         "U_out": (rng.standard_normal((m.V, m.H)) * 0.3).astype(np.float32),
+         "b_out": rng.standard_normal(m.V).astype(np.float32),
+         "maxent": (rng.standard_normal(1 << 12) * 0.5).astype(np.float32)}
+    sc = R.Scorer(m, w, Q_SIGN, max_hist=300, max_query=1)
+    h = np.tanh(rng.standard_normal((300, m.H))).astype(np.float32)
+    words = rng.integers(0, m.V, (300, 3)).astype(np.int32)
+    words[:5] = 0   # sentence start context
+    z = sc.log_normalizer_maxent(torch.from_numpy(h).cuda(), torch.from_numpy(words).cuda()).cpu().numpy()
+    want = log_normalizer_maxent(h, w["U_out"], w["b_out"], w["maxent"], words, 4, 12)
+    ok, err = close(z, want, ATOL, RTOL)
+    assert ok, "MaxEnt logZ differs (max err %.3g)" % err
+    assert not np.allclose(z, sc.log_normalizer(torch.from_numpy(h).cuda()).cpu().numpy(), atol=1e-3)
+    sc0 = R.Scorer(m, dict(w, maxent=np.zeros(1 << 12, np.float32)), Q_SIGN, max_hist=300, max_query=1)
+    hd, wd = torch.from_numpy(h).cuda(), torch.from_numpy(words).cuda()
+    assert torch.equal(sc0.log_normalizer_maxent(hd, wd), sc0.log_normalizer(hd))
+    wd[7, 1] = m.V + 3
+    sc0.log_normalizer_maxent(hd, wd)
+    assert sc0.stats(check=False)["device_error"] == R.DERR_WORD
+
+
+def test_check_config_maxent_normaliser_sample():
+    """Check-config sizes (V = 200,000, H = 1024, 2^26-entry table), 24 rows."""
+    p = make_pair("check", Q_EXACT, 0, n_frames=1)
+    fr = p.wl.frames[0]
+    rng = np.random.default_rng(4)
+    h = np.tanh(rng.standard_normal((24, p.wl.cfg.model.H))).astype(np.float32)
+    words = fr.hist_words[:24].astype(np.int32)
+    z = p.scorer.log_normalizer_maxent(torch.from_numpy(h).cuda(), torch.from_numpy(words).cuda()).cpu().numpy()
+    m = p.wl.cfg.model
+    want = log_normalizer_maxent(h, p.wl.weights["U_out"], p.wl.weights["b_out"], p.wl.weights["maxent"],
+                                 words, m.maxent_order, m.maxent_log2)
+    ok, err = close(z, want, ATOL, RTOL)
+    assert ok, "MaxEnt logZ differs at check-config size (max err %.3g)" % err

@@ -13,7 +13,7 @@ import pytest
 import scipy.special
 import torch
 
-from oracle import (gru_step, hist_key_hash, log_normalizer, maxent_index,
+from oracle import (gru_step, hist_key_hash, log_normalizer, log_normalizer_maxent, maxent_index,
                     mix64, nce_score)
 
 PHI = 0x9E3779B97F4A7C15
@@ -162,3 +162,35 @@ def test_log_normalizer_closed_forms_and_scipy():
     b = rng.standard_normal(V).astype(np.float32)
     want = scipy.special.logsumexp(h @ U.astype(np.float64).T + b.astype(np.float64), axis=1)
     np.testing.assert_allclose(log_normalizer(h, U, b, chunk=128), want, rtol=1e-14)
+
+
+def test_log_normalizer_maxent_closed_forms_and_brute_force():
+    """MaxEnt-inclusive normaliser: zero weights reduce it to the plain one, a
+    constant table shifts every logit by (orders) * c, and a direct double
+    loop over a tiny vocabulary (math.fsum of exp) agrees."""
+    import math
+    rng = np.random.default_rng(9)
+    V, H, n, log2 = 40, 6, 5, 7
+    h = np.tanh(rng.standard_normal((n, H)))
+    U = rng.standard_normal((V, H)).astype(np.float32)
+    b = rng.standard_normal(V).astype(np.float32)
+    words = rng.integers(0, V, (n, 3))
+    lam = (rng.standard_normal(1 << log2) * 0.5).astype(np.float32)
+    plain = log_normalizer(h, U, b)
+    np.testing.assert_allclose(log_normalizer_maxent(h, U, b, np.zeros(1 << log2, np.float32), words, 4, log2),
+                               plain, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(log_normalizer_maxent(h, U, b, np.full(1 << log2, 0.25, np.float32), words, 4, log2),
+                               plain + 3 * 0.25, rtol=1e-14)
+    got = log_normalizer_maxent(h, U, b, lam, words, 4, log2)
+    for i in range(n):
+        terms = []
+        for v in range(V):
+            a = sum(float(U[v, j]) * h[i, j] for j in range(H)) + float(b[v])
+            for o in range(2, 5):
+                a += float(lam[int(maxent_index(o, [int(words[i, c]) for c in range(o - 1)], v, log2))])
+            terms.append(a)
+        m = max(terms)
+        want = m + math.log(math.fsum(math.exp(t - m) for t in terms))
+        assert abs(got[i] - want) < 1e-12
+    with pytest.raises(ValueError):
+        log_normalizer_maxent(h, U, b, lam, np.full((n, 3), V), 4, log2)
