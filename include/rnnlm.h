@@ -80,9 +80,10 @@ typedef struct {
     int32_t qdigits;       /* significant digits for RNNLM_Q_SIGDIG, 1..3 */
     int32_t max_hist;      /* largest n_hist of any frame, 1..2048 */
     int32_t max_query;     /* largest n_query of any frame, 0..8192 */
-    int32_t pad0;
-    int64_t cap_hist;      /* history-cache entries (admission stops when full) */
-    int64_t cap_query;     /* LM-query cache entries */
+    int32_t sessions;      /* independent decode sessions, 1..8 (0 means 1): each has its own caches and
+                            * statistics, and rnnlm_score_frames scores one frame of each per call */
+    int64_t cap_hist;      /* history-cache entries per session (admission stops when full) */
+    int64_t cap_query;     /* LM-query cache entries per session */
     uint64_t seed;         /* seed of the history-key hash */
 } rnnlm_config;
 
@@ -150,7 +151,18 @@ int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void *workspac
  * when its history key is cached). Asynchronous on `stream`. */
 int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *frame, const rnnlm_out *out, void *stream);
 
-/* Empty both caches, zero the statistics and clear the sticky device flag. */
+/* A block of independent frames in one set of launches (Sec. 4 batches a
+ * frame's queries into one transfer; this batches frames of independent
+ * decoders into one launch): frames[k] (host array of n <= sessions) is the
+ * next frame of session k, scored against session k's caches exactly as
+ * rnnlm_score_frame would, with its outputs in outs[k]. Empty frames take no
+ * part. Sessions share the weights and the launches; with n = 1 this is
+ * rnnlm_score_frame on session 0. Errors as rnnlm_score_frame (a host check
+ * failing for any frame enqueues nothing). */
+int rnnlm_score_frames(rnnlm_t *ctx, const rnnlm_frame *frames, const rnnlm_out *outs, int32_t n, void *stream);
+
+/* Empty both caches of every session, zero the statistics and clear the
+ * sticky device flag. */
 int rnnlm_cache_reset(rnnlm_t *ctx, void *stream);
 
 /* Full-vocabulary log normaliser (the computation NCE avoids, Sec. 2.2):
@@ -170,9 +182,14 @@ int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *log
 int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, const int32_t *words, int32_t n, float *logz,
                                 void *stream);
 
-/* Copy the device statistics into *stats (host memory); synchronises `stream`.
- * Returns RNNLM_EDEVICE if the sticky device flag is set. */
+/* Copy the device statistics, summed over all sessions, into *stats (host
+ * memory); synchronises `stream`. Returns RNNLM_EDEVICE if the sticky device
+ * flag of any session is set (device_error: the OR of all sessions' bits). */
 int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *stats, void *stream);
+
+/* The same for one session (0 <= session < sessions); a device error in any
+ * session still returns RNNLM_EDEVICE. */
+int rnnlm_get_session_stats(rnnlm_t *ctx, int32_t session, rnnlm_stats *stats, void *stream);
 
 /* Test hook: quantise n fp32 elements x with the library's own kernel.
  * codes: EXACT -> uint32[n]; SIGDIG -> uint16[n]; SIGN -> uint64[n/64]

@@ -18,8 +18,10 @@ struct rnnlm_t {
     rnnlm_config cfg;
     rn::Dev dev;
     unsigned host_derr;   // sticky device error as last read by rnnlm_get_stats
-    int pending_parts = 0;   // scoring blocks of the last frame whose counts are not folded yet
-    int staged_max = 0;      // bound on the scores the last frame staged for the LM-query cache
+    // per session: scoring blocks of its last frame whose counts are not
+    // folded yet, and a bound on the scores that frame staged for the cache
+    int pending_parts[rn::kMaxSessions] = {};
+    int staged_max[rn::kMaxSessions] = {};
     // optional per-stage timing (rnnlm_profile)
     uint32_t prof_mask = 0;
     std::vector<std::pair<hipEvent_t, hipEvent_t>> prof_pool;   // created events
@@ -117,6 +119,8 @@ uint32_t pow2_at_least(long long n) {
     return p;
 }
 
+int sessions_of(const rnnlm_config &c) { return c.sessions > 0 ? c.sessions : 1; }
+
 int code_words(const rnnlm_config &c) {
     const int LH = c.L * c.H;
     return c.qmode == RNNLM_Q_SIGN ? LH / 64 : (c.qmode == RNNLM_Q_SIGDIG ? LH / 4 : LH / 2);
@@ -141,6 +145,8 @@ int check_config(const rnnlm_config *c) {
         return fail(RNNLM_EINVAL, "max_query must be 0..%d", rn::kPlanMaxQuery);
     if (c->cap_hist < 0 || c->cap_hist > (1LL << 28)) return fail(RNNLM_EINVAL, "cap_hist out of range");
     if (c->cap_query < 0 || c->cap_query > (1LL << 29)) return fail(RNNLM_EINVAL, "cap_query out of range");
+    if (c->sessions < 0 || c->sessions > rn::kMaxSessions)
+        return fail(RNNLM_EINVAL, "sessions must be 0..%d (0 means 1)", rn::kMaxSessions);
     return RNNLM_OK;
 }
 
@@ -182,8 +188,12 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
             packed[l] = cv.take<char>((size_t)3 * c.H * (Kx + c.H) * welem);
         }
     }
+    d.ln_part = cv.take<float2>((size_t)256 * rn::lognorm_tiles(c.V));
+    // one session's state; sessions 1.. repeat it sess_stride bytes apart
     const size_t mh = c.max_hist, mq = c.max_query > 0 ? c.max_query : 1;
     const size_t ch = c.cap_hist > 0 ? c.cap_hist : 1;
+    cv.off = (cv.off + 255) & ~(size_t)255;
+    const size_t s0 = cv.off;
     d.hc_idx = cv.take<rn::HcIdx>(x.HI);
     d.hc_codes = cv.take<unsigned long long>(ch * CW);
     d.hc_val = cv.take<float>(ch * LH);
@@ -207,17 +217,23 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.f_qrec = cv.take<rn::QRec>(mq);
     d.f_qcand = cv.take<int>(mq);
     d.f_part = cv.take<int4>((mq + 3) / 4);
-    d.ln_part = cv.take<float2>((size_t)256 * rn::lognorm_tiles(c.V));
-    return (cv.off + 255) & ~(size_t)255;
+    const size_t stride = ((cv.off - s0) + 255) & ~(size_t)255;
+    d.sessions = sessions_of(c);
+    d.sess_stride = (long long)stride;
+    return s0 + stride * d.sessions;
 }
 
 // Empty caches (index slot / entry key = -1) and zero counters, with fill
 // kernels rather than memsets so the sequence can live in a captured graph.
 void reset_state(const rn::Dev &d, const Extents &x, hipStream_t s) {
-    rn::launch_fill_u32(d.hc_idx, 0xFFFFFFFFu, (long long)x.HI * sizeof(rn::HcIdx) / 4, s);
-    rn::launch_fill_u32(d.sc_tab, 0xFFFFFFFFu, (long long)x.SI * sizeof(rn::ScEnt) / 4, s);
-    rn::launch_fill_u32(d.ctr, 0u, 2LL * rn::C_N, s);
-    rn::launch_fill_u32(d.derr, 0u, 1, s);
+    for (int k = 0; k < d.sessions; ++k) {
+        const long long o = k * d.sess_stride;
+        auto at = [o](void *p) { return static_cast<void *>(static_cast<char *>(p) + o); };
+        rn::launch_fill_u32(at(d.hc_idx), 0xFFFFFFFFu, (long long)x.HI * sizeof(rn::HcIdx) / 4, s);
+        rn::launch_fill_u32(at(d.sc_tab), 0xFFFFFFFFu, (long long)x.SI * sizeof(rn::ScEnt) / 4, s);
+        rn::launch_fill_u32(at(d.ctr), 0u, 2LL * rn::C_N, s);
+        rn::launch_fill_u32(at(d.derr), 0u, 1, s);
+    }
 }
 
 }  // namespace
@@ -278,38 +294,79 @@ RNNLM_API int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void
     return RNNLM_OK;
 }
 
-RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm_out *out, void *stream) {
-    if (!ctx || !fr || !out) return fail(RNNLM_EINVAL, "null context, frame or out");
-    if (ctx->host_derr) return fail(RNNLM_EDEVICE, "sticky device error 0x%x; call rnnlm_cache_reset", ctx->host_derr);
-    const rnnlm_config &c = ctx->cfg;
+// Host checks of one frame; fills f. Returns RNNLM_OK, or 1 for an empty frame.
+static int frame_args(const rnnlm_config &c, const rnnlm_frame *fr, const rnnlm_out *out, rn::FrameArgs &f) {
+    if (!fr || !out) return fail(RNNLM_EINVAL, "null frame or out");
     if (fr->n_hist < 0 || fr->n_hist > c.max_hist) return fail(RNNLM_EINVAL, "n_hist %d outside [0, %d]", fr->n_hist, c.max_hist);
     if (fr->n_query < 0 || fr->n_query > c.max_query) return fail(RNNLM_EINVAL, "n_query %d outside [0, %d]", fr->n_query, c.max_query);
     if (fr->n_query > 0 && fr->n_hist == 0) return fail(RNNLM_EINVAL, "queries without histories");
     if (fr->n_hist > 0 && ((!fr->hist_vec && !fr->hist_ptr) || !fr->hist_words)) return fail(RNNLM_EINVAL, "null history arrays");
     if (fr->n_query > 0 && (!fr->q_hist || !fr->q_tgt || !out->scores)) return fail(RNNLM_EINVAL, "null query arrays or scores");
-    if (fr->n_hist == 0) return RNNLM_OK;
+    if (fr->n_hist == 0) return 1;
     if (!fr->hist_ptr && (reinterpret_cast<uintptr_t>(fr->hist_vec) & 15)) return fail(RNNLM_EINVAL, "hist_vec must be 16-byte aligned");
     if (out->hnew && (reinterpret_cast<uintptr_t>(out->hnew) & 15)) return fail(RNNLM_EINVAL, "hnew must be 16-byte aligned");
-    rn::FrameArgs f;
     f.n_hist = fr->n_hist; f.n_query = fr->n_query;
-    f.hist_vec = fr->hist_vec; f.hist_ptr = reinterpret_cast<const rn::u64 *>(fr->hist_ptr); f.hist_words = fr->hist_words; f.q_hist = fr->q_hist; f.q_tgt = fr->q_tgt;
+    f.hist_vec = fr->hist_vec; f.hist_ptr = reinterpret_cast<const rn::u64 *>(fr->hist_ptr);
+    f.hist_words = fr->hist_words; f.q_hist = fr->q_hist; f.q_tgt = fr->q_tgt;
     f.scores = out->scores; f.hnew = out->hnew; f.q_status = out->q_status; f.h_status = out->h_status;
     f.q_rep = out->q_rep; f.h_rep = out->h_rep; f.h_hash = reinterpret_cast<rn::u64 *>(out->h_hash);
+    return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_score_frames(rnnlm_t *ctx, const rnnlm_frame *frames, const rnnlm_out *outs, int32_t n,
+                                 void *stream) {
+    if (!ctx) return fail(RNNLM_EINVAL, "null context");
+    if (n < 0 || n > ctx->dev.sessions) return fail(RNNLM_EINVAL, "%d frames for %d sessions", n, ctx->dev.sessions);
+    if (n > 0 && (!frames || !outs)) return fail(RNNLM_EINVAL, "null frames or outs");
+    if (ctx->host_derr) return fail(RNNLM_EDEVICE, "sticky device error 0x%x; call rnnlm_cache_reset", ctx->host_derr);
+    const rnnlm_config &c = ctx->cfg;
+    rn::FrameBlock fb;
+    memset(&fb, 0, sizeof fb);
+    int maxh = 0;
+    for (int k = 0; k < n; ++k) {   // frame k belongs to session k; empty frames take no part
+        rn::FrameArgs f;
+        const int rc = frame_args(c, frames + k, outs + k, f);
+        if (rc < 0) return rc;
+        if (rc == 1) continue;
+        const int e = fb.n++;
+        fb.f[e] = f;
+        fb.sess[e] = k;
+        fb.npart[e] = ctx->pending_parts[k];
+        fb.hoff[e + 1] = fb.hoff[e] + (f.n_hist + 3) / 4;
+        fb.qoff[e + 1] = fb.qoff[e] + (f.n_query + 255) / 256;
+        fb.soff[e + 1] = fb.soff[e] + (ctx->staged_max[k] + 255) / 256;
+        fb.qblk[e] = (f.n_query + 3) / 4;
+        fb.boff[e + 1] = fb.boff[e] + fb.qblk[e] + (f.n_hist + 3) / 4;
+        maxh += f.n_hist;
+    }
+    if (fb.n == 0) return RNNLM_OK;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    const rn::Dev &d = ctx->dev;
-    rn::launch_hist_key(d, f, decades(), ctx->staged_max, ctx->pending_parts, s, StageTimer(ctx, 0).ts);
-    ctx->pending_parts = 0;
-    rn::launch_frame_plan(d, f, s, StageTimer(ctx, 1).ts);
+    const int s0 = fb.sess[0];   // the launches see the context from entry 0's session
+    const rn::Dev d = rn::session_view(ctx->dev, s0);
+    int sess_abs[rn::kMaxSessions];
+    for (int e = 0; e < fb.n; ++e) {
+        sess_abs[e] = fb.sess[e];
+        fb.sess[e] -= s0;
+    }
+    rn::launch_hist_key(d, fb, decades(), s, StageTimer(ctx, 0).ts);
+    rn::launch_frame_plan(d, fb, s, StageTimer(ctx, 1).ts);
     {
         const StageTimer t(ctx, 2);
-        for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, f, l, f.n_hist, s, t.part(l, c.L));
+        for (int l = 0; l < c.L; ++l) rn::launch_gru_layer(d, fb, l, maxh, s, t.part(l, c.L));
     }
-    rn::launch_score_finish(d, f, s, StageTimer(ctx, 3).ts);
-    ctx->pending_parts = (f.n_query + 3) / 4;
-    ctx->staged_max = f.n_query;
+    rn::launch_score_finish(d, fb, s, StageTimer(ctx, 3).ts);
+    for (int e = 0; e < fb.n; ++e) {
+        ctx->pending_parts[sess_abs[e]] = (fb.f[e].n_query + 3) / 4;
+        ctx->staged_max[sess_abs[e]] = fb.f[e].n_query;
+    }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "rnnlm_score_frame launch");
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_score_frames launch");
     return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *fr, const rnnlm_out *out, void *stream) {
+    if (!ctx || !fr || !out) return fail(RNNLM_EINVAL, "null context, frame or out");
+    return rnnlm_score_frames(ctx, fr, out, 1, stream);
 }
 
 RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
@@ -318,8 +375,7 @@ RNNLM_API int rnnlm_cache_reset(rnnlm_t *ctx, void *stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "rnnlm_cache_reset launch");
     ctx->host_derr = 0;
-    ctx->pending_parts = 0;
-    ctx->staged_max = 0;
+    for (int k = 0; k < rn::kMaxSessions; ++k) ctx->pending_parts[k] = ctx->staged_max[k] = 0;
     return RNNLM_OK;
 }
 
@@ -353,31 +409,66 @@ RNNLM_API int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, cons
     return log_normalizer(ctx, h_top, words, n, logz, stream, "rnnlm_log_normalizer_maxent launch");
 }
 
-RNNLM_API int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *st, void *stream) {
-    if (!ctx || !st) return fail(RNNLM_EINVAL, "null context or stats");
-    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    long long c[rn::C_N];
-    unsigned derr = 0;
-    rn::launch_fold_stats(ctx->dev, ctx->pending_parts, s);   // counts the last frame's scoring blocks left
-    ctx->pending_parts = 0;
+// Fold every session's pending scoring counts, then read all counters and
+// error words (synchronises).
+static int read_counters(rnnlm_t *ctx, long long (*c)[rn::C_N], unsigned *derr, hipStream_t s) {
+    const rn::Dev &d = ctx->dev;
+    rn::FoldParts fp;
+    for (int k = 0; k < rn::kMaxSessions; ++k) {
+        fp.npart[k] = ctx->pending_parts[k];
+        ctx->pending_parts[k] = 0;
+    }
+    rn::launch_fold_stats(d, fp, s);
     hipError_t e = hipGetLastError();
-    if (e == hipSuccess) e = hipMemcpyAsync(c, ctx->dev.ctr, sizeof c, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(&derr, ctx->dev.derr, sizeof derr, hipMemcpyDeviceToHost, s);
+    for (int k = 0; k < d.sessions && e == hipSuccess; ++k) {
+        const char *base = reinterpret_cast<const char *>(d.ctr) + k * d.sess_stride;
+        e = hipMemcpyAsync(c[k], base, sizeof c[k], hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(derr + k, reinterpret_cast<const char *>(d.derr) + k * d.sess_stride, sizeof(unsigned),
+                               hipMemcpyDeviceToHost, s);
+    }
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "rnnlm_get_stats");
+    return RNNLM_OK;
+}
+
+static void fill_stats(rnnlm_stats *st, const long long *c, unsigned derr) {
+    st->frames += c[rn::C_FRAMES]; st->queries += c[rn::C_QUERIES]; st->score_hits += c[rn::C_SCORE_HITS];
+    st->query_dups += c[rn::C_QUERY_DUPS]; st->computed += c[rn::C_COMPUTED]; st->hists += c[rn::C_HISTS];
+    st->hist_hits += c[rn::C_HIST_HITS]; st->hist_dups += c[rn::C_HIST_DUPS]; st->gru_rows += c[rn::C_GRU_ROWS];
+    st->hist_inserted += c[rn::C_HIST_INS]; st->hist_rejected += c[rn::C_HIST_REJ];
+    st->score_inserted += c[rn::C_SCORE_INS]; st->score_rejected += c[rn::C_SCORE_REJ];
+    st->hist_cache_size += c[rn::C_HC_SIZE]; st->score_cache_size += c[rn::C_SC_SIZE];
+    st->device_error |= (int32_t)derr;
+}
+
+static int stats_of(rnnlm_t *ctx, int session, rnnlm_stats *st, void *stream) {
+    long long c[rn::kMaxSessions][rn::C_N];
+    unsigned derr[rn::kMaxSessions] = {};
+    const int rc = read_counters(ctx, c, derr, reinterpret_cast<hipStream_t>(stream));
+    if (rc) return rc;
     memset(st, 0, sizeof *st);
-    st->frames = c[rn::C_FRAMES]; st->queries = c[rn::C_QUERIES]; st->score_hits = c[rn::C_SCORE_HITS];
-    st->query_dups = c[rn::C_QUERY_DUPS]; st->computed = c[rn::C_COMPUTED]; st->hists = c[rn::C_HISTS];
-    st->hist_hits = c[rn::C_HIST_HITS]; st->hist_dups = c[rn::C_HIST_DUPS]; st->gru_rows = c[rn::C_GRU_ROWS];
-    st->hist_inserted = c[rn::C_HIST_INS]; st->hist_rejected = c[rn::C_HIST_REJ];
-    st->score_inserted = c[rn::C_SCORE_INS]; st->score_rejected = c[rn::C_SCORE_REJ];
-    st->hist_cache_size = c[rn::C_HC_SIZE]; st->score_cache_size = c[rn::C_SC_SIZE];
-    st->device_error = (int32_t)derr;
-    if (derr) {
-        ctx->host_derr = derr;
-        return fail(RNNLM_EDEVICE, "device error bits 0x%x", derr);
+    unsigned all = 0;
+    for (int k = 0; k < ctx->dev.sessions; ++k) {
+        all |= derr[k];
+        if (session < 0 || session == k) fill_stats(st, c[k], derr[k]);
+    }
+    if (all) {   // sticky for the whole context
+        ctx->host_derr = all;
+        return fail(RNNLM_EDEVICE, "device error bits 0x%x", all);
     }
     return RNNLM_OK;
+}
+
+RNNLM_API int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *st, void *stream) {
+    if (!ctx || !st) return fail(RNNLM_EINVAL, "null context or stats");
+    return stats_of(ctx, -1, st, stream);
+}
+
+RNNLM_API int rnnlm_get_session_stats(rnnlm_t *ctx, int32_t session, rnnlm_stats *st, void *stream) {
+    if (!ctx || !st) return fail(RNNLM_EINVAL, "null context or stats");
+    if (session < 0 || session >= ctx->dev.sessions) return fail(RNNLM_EINVAL, "session %d outside [0, %d)", session, ctx->dev.sessions);
+    return stats_of(ctx, session, st, stream);
 }
 
 RNNLM_API int rnnlm_debug_quantize(int32_t qmode, int32_t qdigits, const float *x, int64_t n, void *codes,

@@ -69,10 +69,17 @@ struct QRec {
     int w1, w2, w3;   // w-1 and the key's context words (-1 where unused)
 };
 
-// Everything a kernel needs to know about one context (passed by value).
+// Independent decode sessions per context (one frame each per launch).
+constexpr int kMaxSessions = 8;
+
+// Everything a kernel needs to know about one context (passed by value). The
+// per-session state (caches, counters, per-frame scratch) of session s lives
+// s * sess_stride bytes after session 0's; session_view() shifts the pointers.
 struct Dev {
     // configuration
     int V, E, H, L, LH, wdtype, me_log2, me_order, qmode, qdigits, max_hist, max_query, CW;
+    int sessions;
+    long long sess_stride;
     long long cap_hist, cap_query;
     unsigned long long seed;
     uint32_t hi_mask, si_mask;
@@ -115,6 +122,70 @@ struct Dev {
     // normaliser partials [256][n_tiles] of (max, sum exp)
     float2 *ln_part;
 };
+
+template <class T>
+__host__ __device__ __forceinline__ T *shift_ptr(T *p, long long o) {
+    return reinterpret_cast<T *>(reinterpret_cast<uintptr_t>(p) + o);
+}
+
+// The context as seen by session s: its own caches, counters and scratch.
+// The host applies it to the first frame of a launch, and kernels to later
+// frames relative to that one, so a one-frame launch reads every pointer
+// straight from its arguments.
+__host__ __device__ __forceinline__ Dev session_view(const Dev &d0, int s) {
+    Dev d = d0;
+    const long long o = (long long)s * d0.sess_stride;
+    d.hc_idx = shift_ptr(d.hc_idx, o);
+    d.hc_codes = shift_ptr(d.hc_codes, o);
+    d.hc_val = shift_ptr(d.hc_val, o);
+    d.sc_tab = shift_ptr(d.sc_tab, o);
+    d.sc_stage = shift_ptr(d.sc_stage, o);
+    d.ctr = shift_ptr(d.ctr, o);
+    d.derr = shift_ptr(d.derr, o);
+    d.f_codes = shift_ptr(d.f_codes, o);
+    d.f_hhash = shift_ptr(d.f_hhash, o);
+    d.f_words = shift_ptr(d.f_words, o);
+    d.f_hcslot = shift_ptr(d.f_hcslot, o);
+    d.f_hstat = shift_ptr(d.f_hstat, o);
+    d.f_hslot = shift_ptr(d.f_hslot, o);
+    d.f_hptr = shift_ptr(d.f_hptr, o);
+    d.f_roww = shift_ptr(d.f_roww, o);
+    d.f_rowh = shift_ptr(d.f_rowh, o);
+    d.f_rowdst = shift_ptr(d.f_rowdst, o);
+    d.f_hval = shift_ptr(d.f_hval, o);
+    d.f_qkey = shift_ptr(d.f_qkey, o);
+    d.f_qw1 = shift_ptr(d.f_qw1, o);
+    d.f_qrec = shift_ptr(d.f_qrec, o);
+    d.f_qcand = shift_ptr(d.f_qcand, o);
+    d.f_part = shift_ptr(d.f_part, o);
+    return d;
+}
+
+// The frames of one launch (at most one per session), with each kernel's
+// block ranges: entry e's blocks of a role start at off[e] (off[n] = total).
+struct FrameBlock {
+    FrameArgs f[kMaxSessions];
+    int sess[kMaxSessions];          // session of entry e, relative to entry 0's (the launch's Dev)
+    int n;                           // entries
+    int hoff[kMaxSessions + 1];      // keys kernel: history blocks
+    int qoff[kMaxSessions + 1];      // keys kernel: query-key blocks
+    int soff[kMaxSessions + 1];      // keys kernel: staged-insert blocks
+    int npart[kMaxSessions];         // scoring blocks of the session's last frame still to fold
+    int boff[kMaxSessions + 1];      // scoring kernel: entry e's blocks (its query blocks, then its
+    int qblk[kMaxSessions];          //   qblk[e] = ... history blocks) start at boff[e]
+};
+
+// scoring blocks of each session's last frame whose counts are still to fold
+struct FoldParts {
+    int npart[kMaxSessions];
+};
+
+// entry whose range [off[e], off[e+1]) holds b (off[0] = 0 <= b < off[n])
+__device__ __forceinline__ int entry_of(const int *off, int n, int b) {
+    int e = 0;
+    while (e + 1 < n && b >= off[e + 1]) ++e;
+    return e;
+}
 
 __device__ __forceinline__ u64 mix64(u64 z) {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;

@@ -47,16 +47,63 @@ struct RowSrc {
     bool valid;
 };
 
-__device__ __forceinline__ RowSrc row_source(const Dev &d, const FrameArgs &f, int layer, int m, int M) {
+// The GRU rows of all the launch's frames back to back: entry e's rows are
+// [moff[e], moff[e+1]), and their work lists live in its session's scratch
+// (sofs[e] bytes after session 0's).
+struct Rows {
+    int n;
+    int moff[kMaxSessions + 1];
+    long long sofs[kMaxSessions];
+};
+
+// sessions of the launch's frames (the GRU needs no other frame argument)
+struct SessList {
+    int n;
+    int sess[kMaxSessions];
+};
+
+__device__ __forceinline__ Rows make_rows(const Dev &d, const SessList &sl) {
+    Rows R;
+    R.n = sl.n;
+    int cnt[kMaxSessions];
+#pragma unroll
+    for (int e = 0; e < kMaxSessions; ++e) {   // all counters in flight at once
+        const int ee = e < sl.n ? e : 0;
+        R.sofs[e] = (long long)sl.sess[ee] * d.sess_stride;
+        const long long c = shift_ptr(d.ctr, R.sofs[e])[C_FRAME_M];
+        cnt[e] = e < sl.n ? (int)c : 0;
+    }
+    R.moff[0] = 0;
+#pragma unroll
+    for (int e = 0; e < kMaxSessions; ++e) R.moff[e + 1] = R.moff[e] + cnt[e];
+    return R;
+}
+
+// element `m` (a row of the whole launch) of a per-session work-list array
+template <class T>
+__device__ __forceinline__ T row_at(const Rows &R, T *arr, int m) {
+    if (R.n == 1) return shift_ptr(arr, R.sofs[0])[m];   // one frame (a scalar branch)
+    long long o = R.sofs[0];
+    int base = 0;
+#pragma unroll
+    for (int e = 1; e < kMaxSessions; ++e)   // unrolled selects: no indexed private arrays
+        if (e < R.n && m >= R.moff[e]) {
+            o = R.sofs[e];
+            base = R.moff[e];
+        }
+    return shift_ptr(arr, o)[m - base];
+}
+
+__device__ __forceinline__ RowSrc row_source(const Dev &d, const Rows &R, int layer, int m, int M) {
     RowSrc r;
     r.valid = m < M;
     r.x_bf16 = false;
     r.x = nullptr;
     r.h = nullptr;
     if (!r.valid) return r;
-    r.h = reinterpret_cast<const float *>(d.f_rowh[m]) + (size_t)layer * d.H;
+    r.h = reinterpret_cast<const float *>(row_at(R, d.f_rowh, m)) + (size_t)layer * d.H;
     if (layer == 0) {
-        const int w = d.f_roww[m];   // loaded beside f_rows, not after it
+        const int w = row_at(R, d.f_roww, m);
         if (d.wdtype == RNNLM_BF16) {
             r.x = reinterpret_cast<const uint16_t *>(d.emb) + (size_t)w * d.E;
             r.x_bf16 = true;
@@ -64,12 +111,12 @@ __device__ __forceinline__ RowSrc row_source(const Dev &d, const FrameArgs &f, i
             r.x = reinterpret_cast<const float *>(d.emb) + (size_t)w * d.E;
         }
     } else {
-        r.x = reinterpret_cast<const float *>(d.f_rowdst[m]) + (size_t)(layer - 1) * d.H;
+        r.x = reinterpret_cast<const float *>(row_at(R, d.f_rowdst, m)) + (size_t)(layer - 1) * d.H;
     }
     return r;
 }
 
-__device__ __forceinline__ void gru_epilogue(const Dev &d, const FrameArgs &f, int layer, int M, int m0,
+__device__ __forceinline__ void gru_epilogue(const Dev &d, const Rows &R, int layer, int M, int m0,
                                              int j0, int rb, int ub, const f4_t &ar, const f4_t &az,
                                              const f4_t &anx, const f4_t &anh) {
     const int lane = threadIdx.x & 63;
@@ -86,8 +133,8 @@ __device__ __forceinline__ void gru_epilogue(const Dev &d, const FrameArgs &f, i
     for (int e = 0; e < 4; ++e) {
         mrow[e] = m0 + rb * 16 + 4 * (lane >> 4) + e;
         const bool ok = mrow[e] < M;
-        src[e] = ok ? reinterpret_cast<const float *>(d.f_rowh[mrow[e]]) : nullptr;
-        dst[e] = ok ? reinterpret_cast<float *>(d.f_rowdst[mrow[e]]) : nullptr;
+        src[e] = ok ? reinterpret_cast<const float *>(row_at(R, d.f_rowh, mrow[e])) : nullptr;
+        dst[e] = ok ? reinterpret_cast<float *>(row_at(R, d.f_rowdst, mrow[e])) : nullptr;
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) hprev[e] = mrow[e] < M ? src[e][(size_t)layer * d.H + j] : 0.0f;
@@ -118,16 +165,19 @@ constexpr int G_LDS_FLOATS = 24576;   // 96 KB
 // Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
 // accumulating the four gate tiles (reset, update, candidate input part,
 // candidate recurrent part) of its K range with MFMAs fed straight from
-// global memory (16 B per lane per operand and step), MD_CH steps in flight
+// global memory (16 B per lane per operand and step), md_ch steps in flight
 // at once, double-buffered; then the partial tiles are summed through LDS and
 // wave 0 applies the gates.
 constexpr int MD_MAXROWS = 256;
-constexpr int MD_CH = 2;
+// steps per chunk: bf16 packs its A operand from two fp32 loads, so it keeps
+// one step per chunk to stay within the register file
+template <bool BF16W>
+constexpr int md_ch() { return BF16W ? 1 : 2; }
 
 template <bool BF16W>
 struct MdOps {
     using T = typename std::conditional<BF16W, uint4, float4>::type;
-    T a[MD_CH], r[MD_CH], z[MD_CH], n[MD_CH];
+    T a[md_ch<BF16W>()], r[md_ch<BF16W>()], z[md_ch<BF16W>()], n[md_ch<BF16W>()];
 };
 
 // one K step of one gate tile: fp32 takes 4 k per lane (four 16x16x4 MFMAs
@@ -143,9 +193,10 @@ __device__ __forceinline__ f4_t md_mfma(uint4 a, uint4 b, f4_t c) {
 }
 
 template <bool BF16W>
-__device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, float *smem) {
+__device__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float *smem) {
     using T = typename MdOps<BF16W>::T;
     using E = typename std::conditional<BF16W, uint16_t, float>::type;
+    constexpr int CH = md_ch<BF16W>();
     const int NJ = d.H / 16;
     const int ntiles = ((M + 15) / 16) * NJ;
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
@@ -166,7 +217,7 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
             jt = tile % NJ;
         }
         const int m0 = mt * 16, j0 = jt * 16;
-        const RowSrc src = row_source(d, f, layer, m0 + row, M);
+        const RowSrc src = row_source(d, R, layer, m0 + row, M);
         const E *pr = Wp + (size_t)(j0 + row) * K + kq, *pz = Wp + (size_t)(d.H + j0 + row) * K + kq,
                 *pn = Wp + (size_t)(2 * d.H + j0 + row) * K + kq;
         auto loadA = [&](int k) -> T {
@@ -182,7 +233,7 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
         };
         auto load = [&](MdOps<BF16W> &o, int sc) {
 #pragma unroll
-            for (int c = 0; c < MD_CH; ++c) {
+            for (int c = 0; c < CH; ++c) {
                 const int st = sc + c;
                 if (st < s1) {
                     const int k = st * KS;
@@ -196,7 +247,7 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
         f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
         auto compute = [&](const MdOps<BF16W> &o, int sc) {
 #pragma unroll
-            for (int c = 0; c < MD_CH; ++c) {
+            for (int c = 0; c < CH; ++c) {
                 const int st = sc + c;
                 if (st < s1) {
                     ar = md_mfma(o.a[c], o.r[c], ar);
@@ -208,11 +259,11 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
         };
         MdOps<BF16W> b0, b1;
         load(b0, s0);
-        for (int sc = s0; sc < s1; sc += 2 * MD_CH) {
-            load(b1, sc + MD_CH);
+        for (int sc = s0; sc < s1; sc += 2 * CH) {
+            load(b1, sc + CH);
             compute(b0, sc);
-            load(b0, sc + 2 * MD_CH);
-            compute(b1, sc + MD_CH);
+            load(b0, sc + 2 * CH);
+            compute(b1, sc + CH);
         }
         // sum the waves' partial tiles, then the gates (wave 0)
         float *red = smem + (size_t)(w * 64 + lane) * 16;
@@ -235,7 +286,7 @@ __device__ void gru_medium(const Dev &d, const FrameArgs &f, int layer, int M, f
                     anh[e] += o[12 + e];
                 }
             }
-            gru_epilogue(d, f, layer, M, m0, j0, 0, 0, ar, az, anx, anh);
+            gru_epilogue(d, R, layer, M, m0, j0, 0, 0, ar, az, anx, anh);
         }
         __syncthreads();   // the partial tiles are reused by the next tile
     }
@@ -256,7 +307,7 @@ constexpr int N_MAXROWS = 32;   // rows handled by the narrow path at most
 constexpr int N_TILES = N_MAXROWS / 16;
 
 template <bool BF16W>
-__device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int g) {
+__device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float *smem, int g) {
     using T = typename MdOps<BF16W>::T;
     using E = typename std::conditional<BF16W, uint16_t, float>::type;
     constexpr int KS = BF16W ? 32 : 16;   // k per step
@@ -281,14 +332,14 @@ __device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, f
         ebr = bb[j];
         ebz = bb[d.H + j];
         ebn = bb[2 * d.H + j];
-        edst = reinterpret_cast<float *>(d.f_rowdst[em]) + (size_t)layer * d.H + j;
-        ehp = reinterpret_cast<const float *>(d.f_rowh[em])[(size_t)layer * d.H + j];
+        edst = reinterpret_cast<float *>(row_at(R, d.f_rowdst, em)) + (size_t)layer * d.H + j;
+        ehp = reinterpret_cast<const float *>(row_at(R, d.f_rowh, em))[(size_t)layer * d.H + j];
     }
-    constexpr int PASS = 12;              // steps whose operands are loaded together
+    constexpr int PASS = BF16W ? 8 : 12;  // steps whose operands are loaded together (a wave has 6 bf16 steps at K = 1536)
     T b[PASS];
     RowSrc src[N_TILES];
 #pragma unroll
-    for (int t = 0; t < N_TILES; ++t) src[t] = row_source(d, f, layer, 16 * t + col, M);
+    for (int t = 0; t < N_TILES; ++t) src[t] = row_source(d, R, layer, 16 * t + col, M);
 
     auto loadA = [&](const RowSrc &rs, int k) -> T {
         if (!rs.valid) return T{0, 0, 0, 0};
@@ -369,7 +420,7 @@ __device__ void gru_narrow(const Dev &d, const FrameArgs &f, int layer, int M, f
 constexpr int F_BK = 32;
 constexpr int F_LDA = F_BK + 4;   // padded LDS row (floats)
 
-__device__ void gru_mfma_f32(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int tile) {
+__device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
     const int NJ = d.H / G_BJ;
     int mt, jt;
     gru_tile_of(tile, NJ, mt, jt);
@@ -386,7 +437,7 @@ __device__ void gru_mfma_f32(const Dev &d, const FrameArgs &f, int layer, int M,
 
     // A loader: row tid/8, 4 consecutive k at (tid%8)*4
     const int a_row = tid >> 3, a_k = (tid & 7) * 4;
-    const RowSrc src = row_source(d, f, layer, m0 + a_row, M);
+    const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
     // B loader: rows (gate, unit) tid/8 and tid/8 + 64
     const int b_k = (tid & 7) * 4;
     const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
@@ -450,7 +501,7 @@ __device__ void gru_mfma_f32(const Dev &d, const FrameArgs &f, int layer, int M,
         if (kt + 1 < nk) store(buf ^ 1);
         __syncthreads();
     }
-    gru_epilogue(d, f, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
+    gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
 }
 
 // ------------------------------- bf16 -------------------------------------
@@ -458,7 +509,7 @@ constexpr int H_BK = 64;
 constexpr int H_LDA = H_BK + 8;   // padded LDS row (bf16 elements)
 
 
-__device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M, float *smem, int tile) {
+__device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
     const int NJ = d.H / G_BJ;
     int mt, jt;
     gru_tile_of(tile, NJ, mt, jt);
@@ -475,7 +526,7 @@ __device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wp[layer]);
 
     const int a_row = tid >> 3, a_k = (tid & 7) * 8;
-    const RowSrc src = row_source(d, f, layer, m0 + a_row, M);
+    const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
     const int b_k = (tid & 7) * 8;
     const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
     const uint16_t *bp0 = Wp + (size_t)((b_r0 / G_BJ) * d.H + j0 + (b_r0 % G_BJ)) * K + b_k;
@@ -533,7 +584,7 @@ __device__ void gru_mfma_bf16(const Dev &d, const FrameArgs &f, int layer, int M
         if (kt + 1 < nk) store(buf ^ 1);
         __syncthreads();
     }
-    gru_epilogue(d, f, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
+    gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
 }
 
 // One launch per layer; the device-side row count picks the path.
@@ -543,24 +594,25 @@ static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS 
 static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
 template <bool BF16W>
-__global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, FrameArgs f, int layer) {
+__global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer) {
     __shared__ __align__(16) float smem[G_LDS_FLOATS];
-    const int M = (int)d.ctr[C_FRAME_M];
+    const Rows R = make_rows(d, sl);
+    const int M = R.moff[kMaxSessions];   // rows of all the launch's frames
     if (M <= 0) return;
     if (M <= N_MAXROWS) {             // few rows: every CU streams its share of the weights
         const int NB = d.H / 4;
         for (int t = blockIdx.x; t < NB; t += gridDim.x) {
             const int g = (NB & 7) == 0 && (int)gridDim.x >= NB ? (t & 7) * (NB >> 3) + (t >> 3) : t;
             __syncthreads();
-            gru_narrow<BF16W>(d, f, layer, M, smem, g);
+            gru_narrow<BF16W>(d, R, layer, M, smem, g);
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
-        gru_medium<BF16W>(d, f, layer, M, smem);
+        gru_medium<BF16W>(d, R, layer, M, smem);
     } else {                          // 64 x 32 MFMA tiles through LDS
         const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / G_BJ);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (BF16W) gru_mfma_bf16(d, f, layer, M, smem, t);
-            else gru_mfma_f32(d, f, layer, M, smem, t);
+            if (BF16W) gru_mfma_bf16(d, R, layer, M, smem, t);
+            else gru_mfma_f32(d, R, layer, M, smem, t);
         }
     }
 }
@@ -593,14 +645,17 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
                                        d.wdtype == RNNLM_BF16 ? 2 : 4);
 }
 
-void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s, Stamp ts) {
+void launch_gru_layer(const Dev &d, const FrameBlock &fb, int layer, int max_rows, hipStream_t s, Stamp ts) {
     if (max_rows <= 0) return;
+    SessList sl;
+    sl.n = fb.n;
+    for (int e = 0; e < kMaxSessions; ++e) sl.sess[e] = e < fb.n ? fb.sess[e] : 0;
     // one block per CU (the LDS buffer allows no more); blocks loop over tiles
     const int blocks = 256;
     if (d.wdtype == RNNLM_BF16)
-        launch_k(k_gru<true>, blocks, G_THREADS, s, ts, d, f, layer);
+        launch_k(k_gru<true>, blocks, G_THREADS, s, ts, d, sl, layer);
     else
-        launch_k(k_gru<false>, blocks, G_THREADS, s, ts, d, f, layer);
+        launch_k(k_gru<false>, blocks, G_THREADS, s, ts, d, sl, layer);
 }
 
 }  // namespace rn

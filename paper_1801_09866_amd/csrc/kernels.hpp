@@ -20,19 +20,17 @@ inline void launch_k(void (*k)(KArgs...), unsigned grid, unsigned block, hipStre
 }
 
 void launch_fill_u32(void *p, uint32_t v, long long n, hipStream_t s);
-void launch_fold_stats(const Dev &d, int npart, hipStream_t s);
-// staged_max: upper bound on the scores the previous frame staged (its query
-// count); npart: its scoring blocks whose counts are still to be folded
-void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, int staged_max, int npart,
-                     hipStream_t s, Stamp ts = {});
-void launch_frame_plan(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts = {});
-void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts = {});
+void launch_fold_stats(const Dev &d, const FoldParts &fp, hipStream_t s);
+// The launches of one frame block (one frame per session, fb.n of them).
+void launch_hist_key(const Dev &d, const FrameBlock &fb, const DecadeTab &T, hipStream_t s, Stamp ts = {});
+void launch_frame_plan(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts = {});
+void launch_score_finish(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts = {});
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s);
 
-// GRU step for the frame's work list, one launch per layer (max_rows bounds
-// the device-side row count).
-void launch_gru_layer(const Dev &d, const FrameArgs &f, int layer, int max_rows, hipStream_t s, Stamp ts = {});
+// GRU step for the work lists of all the block's frames, one launch per layer
+// (max_rows bounds the device-side total row count).
+void launch_gru_layer(const Dev &d, const FrameBlock &fb, int layer, int max_rows, hipStream_t s, Stamp ts = {});
 // concatenate W_ih | W_hh of one layer into the packed [3H][Kx+H] layout
 void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_hh, void *dst,
                        hipStream_t s);

@@ -117,17 +117,9 @@ __device__ void fold_counts(const Dev &d, int npart) {
     }
 }
 
-__global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab T, int hb, int qb, int sb,
-                                                  int npart) {
-    const int b = blockIdx.x;
-    if (b >= hb) {
-        if (b < hb + qb) query_key(d, f, (b - hb) * blockDim.x + threadIdx.x);
-        else if (b < hb + qb + sb) insert_staged(d, b - hb - qb, sb);
-        else fold_counts(d, npart);
-        return;
-    }
+// one wave: history i of a frame
+__device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, int i) {
     const int lane = threadIdx.x & 63;
-    const int i = blockIdx.x * 4 + wave_id();
     if (i >= f.n_hist) return;
     bool hbad = false;   // wave-uniform: one history per wave
     const float *x = hist_row(d, f, i, hbad);
@@ -235,6 +227,41 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d, FrameArgs f, DecadeTab 
     }
 }
 
+// The frames of a launch (one per session) side by side: each role's blocks
+// are split among the frames by the ranges in fb. MULTI = false (a single
+// frame) reads everything at fixed argument offsets, so no argument load
+// waits for another.
+template <bool MULTI>
+__global__ __launch_bounds__(256) void k_hist_key(Dev d0, FrameBlock fb, DecadeTab T) {
+    const int b = blockIdx.x, n = MULTI ? fb.n : 1;
+    const int hb = MULTI ? fb.hoff[n] : fb.hoff[1], qb = MULTI ? fb.qoff[n] : fb.qoff[1],
+              sb = MULTI ? fb.soff[n] : fb.soff[1];
+    int e, lb, role;
+    if (b < hb) {
+        e = MULTI ? entry_of(fb.hoff, n, b) : 0;
+        lb = b - (MULTI ? fb.hoff[e] : 0);
+        role = 0;
+    } else if (b < hb + qb) {
+        e = MULTI ? entry_of(fb.qoff, n, b - hb) : 0;
+        lb = b - hb - (MULTI ? fb.qoff[e] : 0);
+        role = 1;
+    } else if (b < hb + qb + sb) {
+        e = MULTI ? entry_of(fb.soff, n, b - hb - qb) : 0;
+        lb = b - hb - qb - (MULTI ? fb.soff[e] : 0);
+        role = 2;
+    } else {
+        e = MULTI ? b - hb - qb - sb : 0;
+        lb = 0;
+        role = 3;
+    }
+    const Dev d = MULTI ? session_view(d0, fb.sess[e]) : d0;
+    const FrameArgs &f = fb.f[e];
+    if (role == 0) hist_wave(d, f, T, lb * 4 + wave_id());
+    else if (role == 1) query_key(d, f, lb * blockDim.x + threadIdx.x);
+    else if (role == 2) insert_staged(d, lb, fb.soff[e + 1] - fb.soff[e]);
+    else fold_counts(d, fb.npart[e]);
+}
+
 // debug hook: quantise a flat array with the frame kernels' quantiser
 __global__ __launch_bounds__(256) void k_debug_quantize(const float *x, long long n, int qmode, int k,
                                                         DecadeTab T, void *codes, int *err) {
@@ -257,9 +284,12 @@ __global__ __launch_bounds__(256) void k_debug_quantize(const float *x, long lon
     if (bad) atomicOr(err, RNNLM_DERR_VALUE);
 }
 
-__global__ __launch_bounds__(256) void k_fold_stats(Dev d, int npart) {
+// get_stats: block s folds session s's pending scoring counts
+__global__ __launch_bounds__(256) void k_fold_stats(Dev d0, FoldParts fp) {
     __shared__ int s_red[4];
     __shared__ long long c[C_N];
+    const Dev d = session_view(d0, blockIdx.x);
+    const int npart = fp.npart[blockIdx.x];
     if (threadIdx.x < C_N) c[threadIdx.x] = d.ctr[threadIdx.x];
     __syncthreads();
     fold_partials(d, npart, c, s_red);
@@ -282,15 +312,15 @@ void launch_fill_u32(void *p, uint32_t v, long long n, hipStream_t s) {
     k_fill_u32<<<(unsigned)blocks, 256, 0, s>>>(reinterpret_cast<uint32_t *>(p), v, n);
 }
 
-void launch_fold_stats(const Dev &d, int npart, hipStream_t s) {
-    k_fold_stats<<<1, 256, 0, s>>>(d, npart);
+void launch_fold_stats(const Dev &d, const FoldParts &fp, hipStream_t s) {
+    k_fold_stats<<<d.sessions, 256, 0, s>>>(d, fp);
 }
 
-void launch_hist_key(const Dev &d, const FrameArgs &f, const DecadeTab &T, int staged_max, int npart,
-                     hipStream_t s, Stamp ts) {
-    const int hb = (f.n_hist + 3) / 4, qb = (f.n_query + 255) / 256;
-    const int sb = staged_max > 0 ? (staged_max + 255) / 256 : 0;
-    launch_k(k_hist_key, hb + qb + sb + 1, 256, s, ts, d, f, T, hb, qb, sb, npart);
+void launch_hist_key(const Dev &d, const FrameBlock &fb, const DecadeTab &T, hipStream_t s, Stamp ts) {
+    const int n = fb.n;
+    const unsigned grid = fb.hoff[n] + fb.qoff[n] + fb.soff[n] + n;
+    if (n > 1) launch_k(k_hist_key<true>, grid, 256, s, ts, d, fb, T);
+    else launch_k(k_hist_key<false>, grid, 256, s, ts, d, fb, T);
 }
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s) {

@@ -80,7 +80,13 @@ __device__ __forceinline__ u64 frame_query_hash(int rep, int w2, int w3, int t) 
     return mix64(x);
 }
 
-__global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
+// block e plans entry e of the frame block (its session's frame); MULTI =
+// false: one frame, at fixed argument offsets
+template <bool MULTI>
+__global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
+    const int e = MULTI ? (int)blockIdx.x : 0;
+    const Dev d = MULTI ? session_view(d0, fb.sess[e]) : d0;
+    const FrameArgs &f = fb.f[e];
     __shared__ __align__(16) unsigned char s_tab[TAB_BYTES];
     __shared__ int s_rep[kPlanMaxHist];   // representative | status << 16
     __shared__ int s_hsa[kPlanMaxHist];   // cache slot after the frame (-1: not cached)
@@ -374,8 +380,9 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d, FrameArgs f) {
     if (tid < C_N) d.ctr[tid] = c[tid];
 }
 
-void launch_frame_plan(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts) {
-    launch_k(k_frame_plan, 1, PT, s, ts, d, f);
+void launch_frame_plan(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts) {
+    if (fb.n > 1) launch_k(k_frame_plan<true>, fb.n, PT, s, ts, d, fb);
+    else launch_k(k_frame_plan<false>, 1, PT, s, ts, d, fb);
 }
 
 }  // namespace rn

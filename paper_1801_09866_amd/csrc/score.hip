@@ -178,31 +178,39 @@ __device__ void admit_in_order(const Dev &d, const FrameArgs &f, int *s_tmp) {
     }
 }
 
-template <bool BF16>
-__global__ __launch_bounds__(256) void k_score_finish(Dev d, FrameArgs f, int qblocks) {
+// Each frame of the launch owns a contiguous range of blocks: its query
+// blocks, then its history blocks. MULTI = false: one frame, whose range is
+// the whole grid (everything at fixed argument offsets).
+template <bool BF16, bool MULTI>
+__global__ __launch_bounds__(256) void k_score_finish(Dev d0, FrameBlock fb) {
     __shared__ int s_cnt[4];
     __shared__ int s_tmp[8];
     __shared__ int s_last;
+    const int e = MULTI ? entry_of(fb.boff, fb.n, blockIdx.x) : 0;
+    const int b = MULTI ? (int)blockIdx.x - fb.boff[e] : (int)blockIdx.x;   // block within the frame
+    const int nblk = MULTI ? fb.boff[e + 1] - fb.boff[e] : (int)gridDim.x;
+    const int qblocks = fb.qblk[e];
+    const Dev d = MULTI ? session_view(d0, fb.sess[e]) : d0;
+    const FrameArgs &f = fb.f[e];
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const bool near_cap = d.ctr[C_NEAR_CAP] != 0;
     if (tid < 4) s_cnt[tid] = 0;
     __syncthreads();
-    if ((int)blockIdx.x < qblocks) {
-        const int q = blockIdx.x * 4 + w;
+    if (b < qblocks) {
+        const int q = b * 4 + w;
         if (q < f.n_query) score_query<BF16>(d, f, q, lane, near_cap, s_cnt);
     } else {
-        const int i = (blockIdx.x - qblocks) * 4 + w;
+        const int i = (b - qblocks) * 4 + w;
         if (i < f.n_hist) finish_history(d, f, i, lane);
     }
     __syncthreads();
-    if (tid == 0 && (int)blockIdx.x < qblocks)   // folded into the counters by the next planner
-        d.f_part[blockIdx.x] = make_int4(s_cnt[RNNLM_Q_COMPUTED], s_cnt[RNNLM_Q_DUP], s_cnt[RNNLM_Q_SCORE_HIT],
-                                         s_cnt[3]);
-    if (!near_cap) return;   // grid-uniform
-    // last block to finish admits this frame's candidates in order
+    if (tid == 0 && b < qblocks)   // folded into the counters by the next keys kernel
+        d.f_part[b] = make_int4(s_cnt[RNNLM_Q_COMPUTED], s_cnt[RNNLM_Q_DUP], s_cnt[RNNLM_Q_SCORE_HIT], s_cnt[3]);
+    if (!near_cap) return;   // uniform over the frame's blocks
+    // the frame's last block to finish admits its candidates in order
     __threadfence();
     __syncthreads();
-    if (tid == 0) s_last = atomicAdd((unsigned long long *)&d.ctr[C_DONE], 1ull) == (unsigned long long)(gridDim.x - 1);
+    if (tid == 0) s_last = atomicAdd((unsigned long long *)&d.ctr[C_DONE], 1ull) == (unsigned long long)(nblk - 1);
     __syncthreads();
     if (!s_last) return;
     __threadfence();
@@ -210,12 +218,16 @@ __global__ __launch_bounds__(256) void k_score_finish(Dev d, FrameArgs f, int qb
     if (tid == 0) d.ctr[C_DONE] = 0;
 }
 
-void launch_score_finish(const Dev &d, const FrameArgs &f, hipStream_t s, Stamp ts) {
-    const int qb = (f.n_query + 3) / 4, hb = (f.n_hist + 3) / 4;
-    if (d.wdtype == RNNLM_BF16)
-        launch_k(k_score_finish<true>, qb + hb, 256, s, ts, d, f, qb);
-    else
-        launch_k(k_score_finish<false>, qb + hb, 256, s, ts, d, f, qb);
+void launch_score_finish(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts) {
+    const int nb = fb.boff[fb.n];
+    const bool multi = fb.n > 1;
+    if (d.wdtype == RNNLM_BF16) {
+        if (multi) launch_k(k_score_finish<true, true>, nb, 256, s, ts, d, fb);
+        else launch_k(k_score_finish<true, false>, nb, 256, s, ts, d, fb);
+    } else {
+        if (multi) launch_k(k_score_finish<false, true>, nb, 256, s, ts, d, fb);
+        else launch_k(k_score_finish<false, false>, nb, 256, s, ts, d, fb);
+    }
 }
 
 }  // namespace rn

@@ -30,7 +30,7 @@ c_i32, c_i64, c_u64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, cty
 class Config(ctypes.Structure):
     _fields_ = [("V", c_i32), ("E", c_i32), ("H", c_i32), ("L", c_i32), ("wdtype", c_i32),
                 ("maxent_log2", c_i32), ("maxent_order", c_i32), ("qmode", c_i32),
-                ("qdigits", c_i32), ("max_hist", c_i32), ("max_query", c_i32), ("pad0", c_i32),
+                ("qdigits", c_i32), ("max_hist", c_i32), ("max_query", c_i32), ("sessions", c_i32),
                 ("cap_hist", c_i64), ("cap_query", c_i64), ("seed", c_u64)]
 
 
@@ -59,9 +59,10 @@ class Stats(ctypes.Structure):
         return {n: getattr(self, n) for n, _ in self._fields_ if n != "pad"}
 
 
-EXPORTS = ("rnnlm_workspace_size", "rnnlm_create", "rnnlm_score_frame", "rnnlm_cache_reset",
-           "rnnlm_log_normalizer", "rnnlm_log_normalizer_maxent", "rnnlm_get_stats", "rnnlm_debug_quantize", "rnnlm_profile",
-           "rnnlm_profile_read", "rnnlm_destroy", "rnnlm_last_error")
+EXPORTS = ("rnnlm_workspace_size", "rnnlm_create", "rnnlm_score_frame", "rnnlm_score_frames",
+           "rnnlm_cache_reset", "rnnlm_log_normalizer", "rnnlm_log_normalizer_maxent", "rnnlm_get_stats",
+           "rnnlm_get_session_stats", "rnnlm_debug_quantize", "rnnlm_profile", "rnnlm_profile_read",
+           "rnnlm_destroy", "rnnlm_last_error")
 NSTAGES = 10
 STAGES = ("hist_key", "frame_plan", "gru_gemm", "score_finish", "unused4", "unused5",
           "unused6", "unused7", "lognorm_gemm", "lognorm_combine")
@@ -81,6 +82,8 @@ def load(path=LIB_PATH):
     L.rnnlm_workspace_size.argtypes = [P(Config), P(ctypes.c_size_t)]
     L.rnnlm_create.argtypes = [P(Config), P(Weights), c_vp, ctypes.c_size_t, c_vp, P(c_vp)]
     L.rnnlm_score_frame.argtypes = [c_vp, P(Frame), P(Out), c_vp]
+    L.rnnlm_score_frames.argtypes = [c_vp, P(Frame), P(Out), c_i32, c_vp]
+    L.rnnlm_get_session_stats.argtypes = [c_vp, c_i32, P(Stats), c_vp]
     L.rnnlm_cache_reset.argtypes = [c_vp, c_vp]
     L.rnnlm_log_normalizer.argtypes = [c_vp, c_vp, c_i32, c_vp, c_vp]
     L.rnnlm_log_normalizer_maxent.argtypes = [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]
@@ -126,10 +129,10 @@ def _dev(x, dtype, device):
 
 
 def make_config(model, qmode, qdigits=0, max_hist=1024, max_query=8192, cap_hist=1 << 16,
-                cap_query=1 << 20, seed=DEFAULT_SEED):
+                cap_query=1 << 20, seed=DEFAULT_SEED, sessions=1):
     return Config(V=model.V, E=model.E, H=model.H, L=model.L, wdtype=model.wdtype,
                   maxent_log2=model.maxent_log2, maxent_order=model.maxent_order,
-                  qmode=qmode, qdigits=qdigits, max_hist=max_hist, max_query=max_query, pad0=0,
+                  qmode=qmode, qdigits=qdigits, max_hist=max_hist, max_query=max_query, sessions=sessions,
                   cap_hist=cap_hist, cap_query=cap_query, seed=seed)
 
 
@@ -144,11 +147,12 @@ class Scorer:
 
     def __init__(self, model, weights, qmode, qdigits=0, max_hist=1024, max_query=8192,
                  cap_hist=1 << 16, cap_query=1 << 20, seed=DEFAULT_SEED, device="cuda:0",
-                 stream=None):
+                 stream=None, sessions=1):
         L = load()
         self.device = torch.device(device)
         self.model = model
-        self.cfg = make_config(model, qmode, qdigits, max_hist, max_query, cap_hist, cap_query, seed)
+        self.sessions = sessions
+        self.cfg = make_config(model, qmode, qdigits, max_hist, max_query, cap_hist, cap_query, seed, sessions)
         wdt = torch.bfloat16 if model.wdtype == BF16 else torch.float32
         dev = self.device
         self.w = {
@@ -214,6 +218,32 @@ class Scorer:
                                                "h_status", "h_rep", "h_hash")])
         _check(load().rnnlm_score_frame(self.ctx, ctypes.byref(fr), ctypes.byref(co), _stream(stream)))
         return out
+
+    def score_frames(self, frames, outs=None, hnew=True, debug=True, stream=None):
+        """Score one frame per session in one set of launches: frames[k] =
+        (hist_vec, hist_words, q_hist, q_tgt) device tensors of session k
+        (or None for no frame). Returns one output dict per frame."""
+        n = len(frames)
+        fa, oa = (Frame * max(n, 1))(), (Out * max(n, 1))()
+        res = []
+        for k, fr in enumerate(frames):
+            hv, hw, qh, qt = fr if fr is not None else (None, None, None, None)
+            n_h = int(hv.shape[0]) if hv is not None else 0
+            n_q = int(qh.shape[0]) if qh is not None else 0
+            out = outs[k] if outs is not None else self.alloc_out(n_h, n_q, hnew, debug)
+            fa[k] = Frame(n_h, n_q, _ptr(hv), _ptr(hw), _ptr(qh), _ptr(qt), None)
+            oa[k] = Out(*[_ptr(out.get(key)) for key in ("scores", "hnew", "q_status", "q_rep",
+                                                        "h_status", "h_rep", "h_hash")])
+            res.append(out)
+        _check(load().rnnlm_score_frames(self.ctx, fa, oa, n, _stream(stream)))
+        return res
+
+    def session_stats(self, session, stream=None, check=True):
+        s = Stats()
+        rc = load().rnnlm_get_session_stats(self.ctx, session, ctypes.byref(s), _stream(stream))
+        if check:
+            _check(rc)
+        return s.as_dict()
 
     def score_frame_raw(self, frame: Frame, out: Out, stream_ptr: ctypes.c_void_p):
         """Pre-marshalled call (for timing loops)."""

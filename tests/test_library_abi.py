@@ -71,3 +71,24 @@ def test_host_argument_checks_need_no_gpu(lib):
     assert lib.rnnlm_debug_quantize(9, 0, None, 64, None, None, None) == R.EINVAL
     assert lib.rnnlm_debug_quantize(R.Q_SIGN, 0, None, 63, None, None, None) == R.EINVAL
     assert lib.rnnlm_debug_quantize(R.Q_SIGN, 0, None, 0, None, None, None) == R.OK
+
+
+def test_sessions_scale_the_per_session_state(lib):
+    """Sessions share the packed weights and the normaliser scratch; caches,
+    counters and per-frame scratch are repeated per session."""
+    m = CONFIGS["medium"].model
+    size = []
+    for s in (0, 1, 2, 8):
+        cfg = R.make_config(m, R.Q_SIGN, 0, 128, 512, sessions=s)
+        n = ctypes.c_size_t()
+        assert lib.rnnlm_workspace_size(ctypes.byref(cfg), ctypes.byref(n)) == R.OK
+        size.append(n.value)
+    assert size[0] == size[1]                      # 0 means one session
+    per = size[2] - size[1]
+    assert per > 0 and size[3] - size[1] == 7 * per
+    packed = 3 * m.H * (m.E + m.H) * 4
+    assert size[1] - per >= packed                  # the shared part holds the packed weights
+    cfg = R.make_config(m, R.Q_SIGN, 0, 128, 512, sessions=9)
+    assert lib.rnnlm_workspace_size(ctypes.byref(cfg), ctypes.byref(ctypes.c_size_t())) == R.EINVAL
+    assert lib.rnnlm_score_frames(None, None, None, 1, None) == R.EINVAL
+    assert lib.rnnlm_get_session_stats(None, 0, None, None) == R.EINVAL
