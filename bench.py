@@ -47,6 +47,9 @@ def parse():
                     help="time budget of the oracle sample (whole frames from frame 0)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the cpu_baseline leg")
     ap.add_argument("--no-replay", action="store_true", help="skip the per-stage timing replay")
+    ap.add_argument("--sessions", type=int, default=1,
+                    help="independent decode sessions scored one frame each per launch (the workload's "
+                         "frames split into that many consecutive streams)")
     ap.add_argument("--maxent", action="store_true",
                     help="check config: normalise the full output (NCE + MaxEnt logits of every word)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -150,6 +153,8 @@ def main():
         args.steps = cfg.frames - args.warmup
     if cfg.queries == 0:
         return main_check(args, cfg)
+    if args.sessions > 1:
+        return main_sessions(args, cfg)
     qm, qk = qmode_of(args.qmode, cfg)
     n_frames = min(cfg.frames, args.warmup + args.steps)
     W, K = min(args.warmup, n_frames - 1), n_frames - min(args.warmup, n_frames - 1)
@@ -459,6 +464,104 @@ def main_check(args, cfg):
         "roofline": roofline,
         "stages": stages,
         "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def main_sessions(args, cfg):
+    """S independent decode sessions: the workload's frames are split into S
+    consecutive streams (session k gets frames k*F .. k*F + F - 1, its cache
+    starting empty at its first frame), and one launch set scores one frame
+    of every session. A step is one such block of S frames; the value is the
+    queries of all sessions per second."""
+    import torch
+
+    from paper_1801_09866_amd import rnnlm as R
+    from paper_1801_09866_amd.workload import make_workload
+
+    S = args.sessions
+    qm, qk = qmode_of(args.qmode, cfg)
+    F = cfg.frames // S                      # frames per session
+    W = min(args.warmup // S if args.warmup else 0, F - 1)
+    wl = make_workload(args.config, n_frames=F * S)
+    m = cfg.model
+    LH = m.L * m.H
+    dev = torch.device("cuda:0")
+    sc = R.Scorer(m, wl.weights, qm, qk, max_hist=cfg.max_hist, max_query=max(cfg.queries, 1),
+                  cap_hist=cfg.cap_hist, cap_query=cfg.cap_query, device="cuda:0", sessions=S)
+    pool = torch.from_numpy(wl.pool.vec).to(dev)
+    nh = np.array([f.n_hist for f in wl.frames])
+    nq = np.array([f.n_query for f in wl.frames])
+    ho = np.concatenate([[0], np.cumsum(nh)])
+    qo = np.concatenate([[0], np.cumsum(nq)])
+    hv = pool.index_select(0, torch.from_numpy(np.concatenate([f.pool_idx for f in wl.frames])).to(dev))
+    hw = torch.from_numpy(np.concatenate([f.hist_words for f in wl.frames]).astype(np.int32)).to(dev)
+    qh = torch.from_numpy(np.concatenate([f.q_hist for f in wl.frames]).astype(np.int32)).to(dev)
+    qt = torch.from_numpy(np.concatenate([f.q_tgt for f in wl.frames]).astype(np.int32)).to(dev)
+    scores = torch.empty(int(qo[-1]), dtype=torch.float32, device=dev)
+    hnew = torch.empty((int(ho[-1]), LH), dtype=torch.float32, device=dev)
+    del pool
+    blocks = []
+    for j in range(F):                       # block j: frame j of every session
+        fa, oa = (R.Frame * S)(), (R.Out * S)()
+        for k in range(S):
+            i = k * F + j
+            fa[k] = R.Frame(int(nh[i]), int(nq[i]), hv.data_ptr() + int(ho[i]) * LH * 4, hw.data_ptr() + int(ho[i]) * 12,
+                            qh.data_ptr() + int(qo[i]) * 4, qt.data_ptr() + int(qo[i]) * 4, None)
+            oa[k] = R.Out(scores.data_ptr() + int(qo[i]) * 4, hnew.data_ptr() + int(ho[i]) * LH * 4,
+                          None, None, None, None, None)
+        blocks.append((fa, oa))
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    L = R.load()
+    ctx = sc.ctx
+
+    def run(lo, hi):
+        for j in range(lo, hi):
+            rc = L.rnnlm_score_frames(ctx, blocks[j][0], blocks[j][1], S, sp)
+            if rc:
+                raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
+
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    st0 = sc.stats()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    run(W, F)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    gpu_ms = ev0.elapsed_time(ev1)
+    st1 = sc.stats()
+    span = {k: st1[k] - st0[k] for k in st1 if k not in ("hist_cache_size", "score_cache_size", "device_error")}
+    secs = gpu_ms / 1e3
+    queries = span["queries"]
+    value = queries / secs
+    log("timed %d blocks of %d frames: %.3f ms GPU, %.0f queries/s" % (F - W, S, gpu_ms, value))
+    stages = {}
+    if not args.no_replay:
+        sc.reset()
+        run(0, W)
+        sc.profile(R.STAGES[:4])
+        run(W, F)
+        torch.cuda.synchronize()
+        for name, (ms, launches) in sc.profile_read().items():
+            stages[name] = {"ms_total": round(ms, 4), "launches": launches, "us_per_launch": round(1e3 * ms / launches, 2)}
+        sc.profile(())
+        log("stages:", json.dumps(stages))
+    hit = lambda a, b: round(a / b, 4) if b else None
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
+        "steps": F - W, "warmup": W, "ms_per_step": round(gpu_ms / (F - W), 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32" if m.wdtype == 0 else "bf16-weights/f32-accumulate",
+        "data": "synthetic",
+        "config": {"workload": "%s_%s split into %d independent sessions of %d frames, one frame of each per launch"
+                               % (cfg.name, qmode_name(qm, qk), S, F), "sessions": S, "qmode": qmode_name(qm, qk)},
+        "frames_per_s": round(span["frames"] / secs, 1),
+        "computed_queries_per_s": round(span["computed"] / secs, 1),
+        "score_hit_ratio": hit(span["score_hits"], span["queries"]),
+        "hist_hit_ratio": hit(span["hists"] and span["hist_hits"], span["hists"]),
+        "stages": stages, "roofline": None, "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
 
