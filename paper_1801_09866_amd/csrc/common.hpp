@@ -204,18 +204,22 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     return (uint16_t)(u >> 16);
 }
 
-// butterfly sum over the 64 lanes; every lane ends with the same value
-// Address of history i's L*H vector: a row of hist_vec, or its handle. A null
-// or misaligned handle is replaced by a row of the workspace (so no access
-// leaves valid memory) and reported through *bad.
+// A history handle is bad when null or not 16-byte aligned.
+__device__ __forceinline__ bool bad_handle(u64 p) { return p == 0 || (p & 15); }
+
+// The row a history handle names; a bad handle is replaced by a row of the
+// workspace, so that no access leaves valid memory.
+__device__ __forceinline__ const float *handle_row(const Dev &d, u64 p) {
+    return bad_handle(p) ? d.f_hval : reinterpret_cast<const float *>(p);
+}
+
+// Address of history i's L*H vector: a row of hist_vec, or its handle (a bad
+// one is replaced as above and reported through *bad).
 __device__ __forceinline__ const float *hist_row(const Dev &d, const FrameArgs &f, int i, bool &bad) {
     if (!f.hist_ptr) return f.hist_vec + (size_t)i * d.LH;
     const u64 p = f.hist_ptr[i];
-    if (p == 0 || (p & 15)) {
-        bad = true;
-        return d.f_hval;
-    }
-    return reinterpret_cast<const float *>(p);
+    bad = bad_handle(p);
+    return handle_row(d, p);
 }
 
 // Index of the calling wave in its block, as a scalar. The compiler cannot
