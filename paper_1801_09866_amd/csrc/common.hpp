@@ -233,10 +233,15 @@ __device__ __forceinline__ const float *hist_row(const Dev &d, const FrameArgs &
 // the global address space.
 template <typename T>
 __device__ __forceinline__ T ldg(const void *p) {
-    static_assert(sizeof(T) == 16 || sizeof(T) == 8, "16- or 8-byte loads");
-    typedef unsigned int raw __attribute__((ext_vector_type(sizeof(T) / 4)));
-    const raw v = *reinterpret_cast<const __attribute__((address_space(1))) raw *>(reinterpret_cast<uintptr_t>(p));
-    return __builtin_bit_cast(T, v);
+    static_assert(sizeof(T) == 16 || sizeof(T) == 8 || sizeof(T) == 4, "16-, 8- or 4-byte loads");
+    if constexpr (sizeof(T) == 4) {
+        const unsigned v = *reinterpret_cast<const __attribute__((address_space(1))) unsigned *>(reinterpret_cast<uintptr_t>(p));
+        return __builtin_bit_cast(T, v);
+    } else {
+        typedef unsigned int raw __attribute__((ext_vector_type(sizeof(T) / 4)));
+        const raw v = *reinterpret_cast<const __attribute__((address_space(1))) raw *>(reinterpret_cast<uintptr_t>(p));
+        return __builtin_bit_cast(T, v);
+    }
 }
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }

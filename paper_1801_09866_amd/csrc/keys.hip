@@ -6,34 +6,38 @@
 
 namespace rn {
 
-__constant__ u64 kPow5[23] = {
-    1ull, 5ull, 25ull, 125ull, 625ull, 3125ull, 15625ull, 78125ull, 390625ull, 1953125ull,
-    9765625ull, 48828125ull, 244140625ull, 1220703125ull, 6103515625ull, 30517578125ull,
-    152587890625ull, 762939453125ull, 3814697265625ull, 19073486328125ull, 95367431640625ull,
-    476837158203125ull, 2384185791015625ull};
-__constant__ uint32_t kPow10[4] = {1u, 10u, 100u, 1000u};
-
 // k-significant-digit code of one fp32 element (Sec. 3 "rounding"), ties away
 // from zero. Code = sign<<15 | (e+20)<<10 | m for +-m*10^(e-k+1), zero -> 0.
 // |x| = M * 2^-s; the decade e = -j is found by comparing bit patterns with
 // the exact decade boundaries, then m = floor(M*10^p/2^s + 1/2) with
-// 10^p = 5^p * 2^p evaluated in 128-bit integers.
+// 10^p = 5^p * 2^p evaluated in 128-bit integers. Everything is computed in
+// registers: the boundaries are uniform (one comparison each, no per-lane
+// table index) and 5^p is a product of 5^(2^b) over the bits b of p.
 __device__ __forceinline__ uint32_t sigdig_code(float x, int k, const DecadeTab &T, bool &bad) {
     uint32_t b = __float_as_uint(x);
     uint32_t neg = b >> 31, mag = b & 0x7FFFFFFFu;
     if (mag > 0x3F800000u) { bad = true; return 0u; }   // |x| > 1, inf, nan
     if (mag < T.lo[20]) return 0u;                       // |x| < 1e-20
+    // 10^-j <= |x| < 10^(1-j): the boundaries decrease with j, so j counts
+    // the boundaries above |x|
     int j = 0;
-    while (mag < T.lo[j]) ++j;                           // 10^-j <= |x| < 10^(1-j)
+#pragma unroll
+    for (int c = 0; c < 20; ++c) j += mag < T.lo[c] ? 1 : 0;
     uint32_t ex = mag >> 23;                             // normal: |x| >= 1e-20
     u64 M = (u64)((mag & 0x7FFFFFu) | 0x800000u);
     int s = 150 - (int)ex;
-    int p = k - 1 + j;
+    int p = k - 1 + j;                                   // 0 .. 22
+    u64 pow5 = (p & 1) ? 5ull : 1ull;
+    pow5 *= (p & 2) ? 25ull : 1ull;
+    pow5 *= (p & 4) ? 625ull : 1ull;
+    pow5 *= (p & 8) ? 390625ull : 1ull;
+    pow5 *= (p & 16) ? 152587890625ull : 1ull;
     int sh = s - p;                                      // >= 18 for |x| <= 1
-    unsigned __int128 v = (unsigned __int128)M * kPow5[p] + ((unsigned __int128)1 << (sh - 1));
+    unsigned __int128 v = (unsigned __int128)M * pow5 + ((unsigned __int128)1 << (sh - 1));
     uint32_t m = (uint32_t)(v >> sh);
     int e = -j;
-    if (m == kPow10[k]) { m = kPow10[k - 1]; e += 1; }
+    const uint32_t top = k == 1 ? 10u : k == 2 ? 100u : 1000u;   // 10^k
+    if (m == top) { m = top / 10u; e += 1; }
     return (neg << 15) | ((uint32_t)(e + 20) << 10) | m;
 }
 
@@ -56,6 +60,7 @@ __device__ __forceinline__ bool nonfinite(float x) {
 //   EXACT  word w = elements 2w, 2w+1, held by lane w % 64, slot w / 64
 // ---------------------------------------------------------------------------
 constexpr int kWordsPerLane = kMaxCW / 64;   // 16
+constexpr int kSignWords = kMaxLH / 64;      // sign code words of the longest vector
 
 // Block roles (independent work, so one launch runs them side by side):
 //   [0, hb)            one wave per history (below)
@@ -121,6 +126,10 @@ __device__ void fold_counts(const Dev &d, int npart) {
 __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, int i) {
     const int lane = threadIdx.x & 63;
     if (i >= f.n_hist) return;
+    // the record's words are loaded with the row, not after it
+    int w3[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) w3[c] = f.hist_words[(size_t)i * 3 + c];
     bool hbad = false;   // wave-uniform: one history per wave
     const float *x = hist_row(d, f, i, hbad);
     const int CW = d.CW;
@@ -128,41 +137,49 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     bool bad = false;
     u64 hs = 0;
     if (d.qmode == RNNLM_Q_SIGN) {
+        // the whole row in flight at once (one coalesced load per 64
+        // elements), then one ballot per code word
+        float v[kSignWords];
+#pragma unroll
+        for (int u = 0; u < kSignWords; ++u) v[u] = u < CW ? ldg<float>(x + u * 64 + lane) : 0.0f;
         words[0] = 0;
-        for (int w0 = 0; w0 < CW; w0 += 8) {   // 8 coalesced loads in flight, then 8 ballots
-            float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = w0 + u < CW ? x[(w0 + u) * 64 + lane] : 0.0f;
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                if (w0 + u < CW) {   // wave-uniform
-                    bad |= nonfinite(v[u]);
-                    const u64 b = __ballot(v[u] < 0.0f);
-                    if (lane == w0 + u) words[0] = b;
-                }
+        for (int u = 0; u < kSignWords; ++u) {
+            if (u < CW) {   // wave-uniform
+                bad |= nonfinite(v[u]);
+                const u64 b = __ballot(v[u] < 0.0f);
+                if (lane == u) words[0] = b;
             }
         }
         if (lane < CW) hs = mix64(words[0] ^ ((u64)(lane + 1) * kPhi));
     } else if (d.qmode == RNNLM_Q_SIGDIG) {
+        // all of the row's loads first (4 elements per code word), then the codes
+        float4 v[kWordsPerLane / 2];
+#pragma unroll
+        for (int s = 0; s < kWordsPerLane / 2; ++s)
+            v[s] = lane + 64 * s < CW ? ldg<float4>(x + 4 * (lane + 64 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int s = 0; s < kWordsPerLane / 2; ++s) {
             const int w = lane + 64 * s;
             if (w < CW) {
-                const float4 v = reinterpret_cast<const float4 *>(x)[w];
-                words[s] = (u64)sigdig_code(v.x, d.qdigits, T, bad) |
-                           ((u64)sigdig_code(v.y, d.qdigits, T, bad) << 16) |
-                           ((u64)sigdig_code(v.z, d.qdigits, T, bad) << 32) |
-                           ((u64)sigdig_code(v.w, d.qdigits, T, bad) << 48);
+                words[s] = (u64)sigdig_code(v[s].x, d.qdigits, T, bad) |
+                           ((u64)sigdig_code(v[s].y, d.qdigits, T, bad) << 16) |
+                           ((u64)sigdig_code(v[s].z, d.qdigits, T, bad) << 32) |
+                           ((u64)sigdig_code(v[s].w, d.qdigits, T, bad) << 48);
                 hs += mix64(words[s] ^ ((u64)(w + 1) * kPhi));
             }
         }
     } else {
+        // all of the row's loads first (2 elements per code word), then the codes
+        float2 v[kWordsPerLane];
+#pragma unroll
+        for (int s = 0; s < kWordsPerLane; ++s)
+            v[s] = lane + 64 * s < CW ? ldg<float2>(x + 2 * (lane + 64 * s)) : make_float2(0.f, 0.f);
 #pragma unroll
         for (int s = 0; s < kWordsPerLane; ++s) {
             const int w = lane + 64 * s;
             if (w < CW) {
-                const float2 v = reinterpret_cast<const float2 *>(x)[w];
-                words[s] = (u64)exact_code(v.x, bad) | ((u64)exact_code(v.y, bad) << 32);
+                words[s] = (u64)exact_code(v[s].x, bad) | ((u64)exact_code(v[s].y, bad) << 32);
                 hs += mix64(words[s] ^ ((u64)(w + 1) * kPhi));
             }
         }
@@ -173,12 +190,9 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     // words of the history record (validated, clamped)
     // a bad handle read a placeholder row: report the handle, not its values
     unsigned err = hbad ? RNNLM_DERR_HANDLE : (anybad ? RNNLM_DERR_VALUE : 0u);
-    int w3[3];
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
-        w3[c] = f.hist_words[(size_t)i * 3 + c];
+    for (int c = 0; c < 3; ++c)
         if (w3[c] < 0 || w3[c] >= d.V) { err |= RNNLM_DERR_WORD; w3[c] = 0; }
-    }
     const int w1 = w3[0];
     const u64 h = mix64(d.seed ^ S ^ mix64((u64)w1 + 1));
 
