@@ -19,6 +19,8 @@
 
 namespace rn {
 
+constexpr int kRowSteps = kMaxLH / 256;   // 16-byte fp32 steps per lane over the longest row
+
 // staging slot e receives a new LM-query cache entry (hs = -1: slot unused)
 __device__ __forceinline__ void stage_score(const Dev &d, long long e, int hs, int w2, int w3, int t, float s) {
     ScEnt en;
@@ -36,51 +38,74 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
                                             int *s_cnt) {
     const QRec rec = d.f_qrec[q];
     const int t = rec.t;
+    const bool probe = rec.flags & QF_PROBE;   // wave-uniform: one query per wave
+    // Once the record is in, everything the query can need is loaded at
+    // once: the LM cache's first probe record (for a cached history key), the
+    // output row, the history row, the bias and the MaxEnt weights. A hit
+    // wastes the row loads but saves the round trip a miss would wait for.
+    unsigned pos = (unsigned)(query_hash((u64)rec.hs, rec.w2, rec.w3, t) & d.si_mask);
+    ScEnt e = d.sc_tab[probe ? pos : 0];
+    const float *h = reinterpret_cast<const float *>(rec.hptr);
+    float acc = 0.0f;
+    if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
+        const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
+        float4 a[kRowSteps], b[kRowSteps];
+#pragma unroll
+        for (int st = 0; st < kRowSteps; ++st) {
+            const int k = lane * 4 + st * 256;
+            a[st] = b[st] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k < d.H) {
+                a[st] = ldg<float4>(u + k);
+                b[st] = ldg<float4>(h + k);
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < kRowSteps; ++st) {
+            acc = fmaf(a[st].x, b[st].x, acc);
+            acc = fmaf(a[st].y, b[st].y, acc);
+            acc = fmaf(a[st].z, b[st].z, acc);
+            acc = fmaf(a[st].w, b[st].w, acc);
+        }
+    } else {   // 8 bf16 weights per lane per 512 elements
+        const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
+        uint4 a[kRowSteps / 2];
+        float4 b0[kRowSteps / 2], b1[kRowSteps / 2];
+#pragma unroll
+        for (int st = 0; st < kRowSteps / 2; ++st) {
+            const int k = lane * 8 + st * 512;
+            a[st] = make_uint4(0u, 0u, 0u, 0u);
+            b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k < d.H) {
+                a[st] = ldg<uint4>(u + k);
+                b0[st] = ldg<float4>(h + k);
+                b1[st] = ldg<float4>(h + k + 4);
+            }
+        }
+#pragma unroll
+        for (int st = 0; st < kRowSteps / 2; ++st) {
+            acc = fmaf(__uint_as_float(a[st].x << 16), b0[st].x, acc);
+            acc = fmaf(__uint_as_float(a[st].x & 0xFFFF0000u), b0[st].y, acc);
+            acc = fmaf(__uint_as_float(a[st].y << 16), b0[st].z, acc);
+            acc = fmaf(__uint_as_float(a[st].y & 0xFFFF0000u), b0[st].w, acc);
+            acc = fmaf(__uint_as_float(a[st].z << 16), b1[st].x, acc);
+            acc = fmaf(__uint_as_float(a[st].z & 0xFFFF0000u), b1[st].y, acc);
+            acc = fmaf(__uint_as_float(a[st].w << 16), b1[st].z, acc);
+            acc = fmaf(__uint_as_float(a[st].w & 0xFFFF0000u), b1[st].w, acc);
+        }
+    }
+    float me = d.b_out[t];
+    for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, rec.w1, rec.w2, rec.w3, t, d.me_log2)];
     bool hit = false;
     float s = 0.0f;
-    if (rec.flags & QF_PROBE) {
-        unsigned pos = (unsigned)(query_hash((u64)rec.hs, rec.w2, rec.w3, t) & d.si_mask);
+    if (probe) {
         for (unsigned k = 0; k <= d.si_mask; ++k) {
-            const ScEnt e = d.sc_tab[pos];
             if (e.hs < 0) break;
             if (e.hs == rec.hs && e.w2 == rec.w2 && e.w3 == rec.w3 && e.t == t) { hit = true; s = e.val; break; }
             pos = (pos + 1) & d.si_mask;
+            e = d.sc_tab[pos];
         }
     }
-    if (!hit) {
-        const float *h = reinterpret_cast<const float *>(rec.hptr);
-        float acc = 0.0f;
-        if (!BF16) {
-            const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
-            for (int e = lane * 4; e < d.H; e += 256) {
-                const float4 a = ldg<float4>(u + e);
-                const float4 b = ldg<float4>(h + e);
-                acc = fmaf(a.x, b.x, acc);
-                acc = fmaf(a.y, b.y, acc);
-                acc = fmaf(a.z, b.z, acc);
-                acc = fmaf(a.w, b.w, acc);
-            }
-        } else {
-            const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
-            for (int e = lane * 8; e < d.H; e += 512) {
-                const uint4 a = ldg<uint4>(u + e);
-                const float4 b0 = ldg<float4>(h + e);
-                const float4 b1 = ldg<float4>(h + e + 4);
-                acc = fmaf(__uint_as_float(a.x << 16), b0.x, acc);
-                acc = fmaf(__uint_as_float(a.x & 0xFFFF0000u), b0.y, acc);
-                acc = fmaf(__uint_as_float(a.y << 16), b0.z, acc);
-                acc = fmaf(__uint_as_float(a.y & 0xFFFF0000u), b0.w, acc);
-                acc = fmaf(__uint_as_float(a.z << 16), b1.x, acc);
-                acc = fmaf(__uint_as_float(a.z & 0xFFFF0000u), b1.y, acc);
-                acc = fmaf(__uint_as_float(a.w << 16), b1.z, acc);
-                acc = fmaf(__uint_as_float(a.w & 0xFFFF0000u), b1.w, acc);
-            }
-        }
-        // MaxEnt weights and bias are loaded while the row is in flight
-        float me = d.b_out[t];
-        for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, rec.w1, rec.w2, rec.w3, t, d.me_log2)];
-        s = wave_sum(acc) + me;
-    }
+    if (!hit) s = wave_sum(acc) + me;
     if (lane == 0) {
         const int st = hit ? RNNLM_Q_SCORE_HIT : (rec.flags & 3);
         f.scores[q] = s;
@@ -118,10 +143,16 @@ __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f,
             }
         }
     }
-    if (f.hnew) {
+    if (f.hnew) {   // the whole row in flight, then stored
         const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
         float4 *dst = reinterpret_cast<float4 *>(f.hnew + (size_t)i * d.LH);
-        for (int e = lane; e < d.LH / 4; e += 64) dst[e] = ldg<float4>(src + e);
+        float4 v[kRowSteps];
+#pragma unroll
+        for (int st = 0; st < kRowSteps; ++st)
+            if (lane + 64 * st < d.LH / 4) v[st] = ldg<float4>(src + lane + 64 * st);
+#pragma unroll
+        for (int st = 0; st < kRowSteps; ++st)
+            if (lane + 64 * st < d.LH / 4) dst[lane + 64 * st] = v[st];
     }
 }
 
