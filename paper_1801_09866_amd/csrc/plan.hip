@@ -11,8 +11,9 @@
 // lowers its slot of a table to (fingerprint, index) with one atomic min;
 // after a barrier it reads the slot back. The smallest fingerprint at a slot
 // keeps it, with its lowest index; the other keys at that slot race again in
-// a smaller table at a position drawn from their fingerprint, and the few
-// left after the last table resolve by an exact scan. Every round is
+// a smaller table at a position drawn from their fingerprint; the few left
+// after the last table settle in a small probed table, and any left over
+// from that resolve by an exact scan. Every round is
 // branch-free and ends with one barrier, so the cost is a few short LDS
 // rounds instead of probe chains of dependent atomics. A settled key's
 // representative is confirmed by an exact key comparison, so a fingerprint
@@ -38,6 +39,7 @@ constexpr int HW = kPlanMaxHist / 64;              // history flag words
 constexpr int QW = kPlanMaxQuery / 64;             // query flag words
 constexpr int KR = 4;                              // race rounds (tables per kind)
 constexpr int HIB = 11, QIB = 13;                  // index bits in a history / query slot
+constexpr int OVF = 128;                           // overflow table slots per kind
 static_assert(kPlanMaxHist <= (1 << HIB) && kPlanMaxQuery <= (1 << QIB), "slot index fields too narrow");
 static_assert(QW <= 128, "flag prefix covers two words per lane");
 static_assert(kPlanMaxHist <= 65536, "representatives are packed in 16 bits");
@@ -135,6 +137,24 @@ __device__ __forceinline__ int flag_rank(const u64 *words, const int *pre, int e
     return pre[e >> 6] + __popcll(words[e >> 6] & ((1ull << lane) - 1ull));
 }
 
+// Insert value v (fingerprint above `ib` index bits) of a key whose hash has
+// low word lo into an overflow table of OVF slots (empty: all ones): a slot
+// holding the same fingerprint keeps the lower index. Returns the slot, or
+// OVF when the table is full.
+__device__ __forceinline__ unsigned overflow_insert(uint32_t *t, uint32_t lo, uint32_t v, int ib) {
+    unsigned pos = lo & (OVF - 1);
+    for (int k = 0; k < OVF; ++k) {
+        const uint32_t old = atomicCAS(&t[pos], 0xFFFFFFFFu, v);
+        if (old == 0xFFFFFFFFu) return pos;
+        if ((old >> ib) == (v >> ib)) {
+            atomicMin(&t[pos], v);
+            return pos;
+        }
+        pos = (pos + 1) & (OVF - 1);
+    }
+    return OVF;
+}
+
 // In-frame placement hash of a query key: its history's key hash (folded to
 // 32 bits), context words and target, mixed once. Equal keys hash equally;
 // the exact check catches every collision.
@@ -162,6 +182,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
     __shared__ int s_cnt[2];
     __shared__ int s_htot, s_qtot;
     __shared__ int s_more[3];          // race rounds: some key lost in round k (k mod 3)
+    __shared__ uint32_t s_ovf[2 * OVF];  // keys still racing after the last table: histories, then queries
 
     const int tid = threadIdx.x, lane = tid & 63, n = f.n_hist, nq = f.n_query;
     const int RQ = (nq + PT - 1) / PT;    // active query rounds (block-uniform)
@@ -203,6 +224,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
     int tab_slots = 0;
     const Race HRc = race_layout(S0, tab_slots);
     const Race QRc = race_layout(RQ > 0 ? Q0 : 0, tab_slots);
+    if (tid < 2 * OVF) s_ovf[tid] = 0xFFFFFFFFu;
     for (int k = tid; k < tab_slots / 4; k += PT)   // slot counts are multiples of 64
         reinterpret_cast<uint4 *>(tab)[k] = make_uint4(0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu);
     if (tid < 2) s_cnt[tid] = 0;
@@ -298,11 +320,39 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
             }
             lost |= lose;
         }
-        if (!more) break;
         if (__any(lost) && (tid & 63) == 0) s_more[k % 3] = 1;
         if (tid == 0) s_more[(k + 1) % 3] = 0;
         __syncthreads();
         if (!s_more[k % 3]) break;   // block-uniform: nobody lost
+        if (more) continue;
+        // Keys still racing after the last table (rare): open addressing in
+        // a small table of their own (compare-and-swap probing; few keys,
+        // short chains), where a fingerprint again keeps its lowest index.
+        // A key that finds no slot stays racing and takes the exact scan.
+        unsigned hop[HR], qop[QR];
+#pragma unroll
+        for (int r = 0; r < HR; ++r) {
+            hop[r] = OVF;
+            if ((hpend >> r) & 1u) hop[r] = overflow_insert(s_ovf, hlo[r], hv[r], HIB);
+        }
+#pragma unroll
+        for (int r = 0; r < QR; ++r) {
+            qop[r] = OVF;
+            if (r < RQ && ((qpend >> r) & 1u)) qop[r] = overflow_insert(s_ovf + OVF, qlo[r], qv[r], QIB);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < HR; ++r)
+            if (hop[r] < OVF) {
+                hmin[r] = (int)(s_ovf[hop[r]] & ((1u << HIB) - 1));
+                hpend &= ~(1u << r);
+            }
+#pragma unroll
+        for (int r = 0; r < QR; ++r)
+            if (qop[r] < OVF) {
+                qmin[r] = (int)(s_ovf[OVF + qop[r]] & ((1u << QIB) - 1));
+                qpend &= ~(1u << r);
+            }
     }
 
     // ---------------- history representatives and statuses ----------------
