@@ -7,7 +7,9 @@
 The first form prints, per kernel: calls, average duration; and for counter
 runs the mean of every collected counter per dispatch. With --copy-bytes, the
 counters of the plain copy kernel in the run are used to print a
-bytes-per-counter-unit scale factor.
+bytes-per-counter-unit scale factor. With --dispatches NAME, it also lists
+the counters of every dispatch of the kernels whose name contains NAME, in
+dispatch order.
 
 The second form prints one line per library kernel,
     traffic WORKLOAD STAGE fetch_bytes=F write_bytes=W source_sha256=S
@@ -43,6 +45,21 @@ def counters(d):
             for r in csv.DictReader(f):
                 acc[r["Kernel_Name"]][r["Counter_Name"]].append(float(r["Counter_Value"]))
     return acc
+
+
+def dispatches(d, name):
+    """Counter values of each dispatch of the kernels matching `name`:
+    [(dispatch id, kernel, {counter: value})] in dispatch order."""
+    rows = collections.defaultdict(dict)
+    kern = {}
+    for p in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(p) as f:
+            for r in csv.DictReader(f):
+                if name in r["Kernel_Name"]:
+                    i = int(r["Dispatch_Id"])
+                    rows[i][r["Counter_Name"]] = rows[i].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                    kern[i] = r["Kernel_Name"]
+    return [(i, kern[i], rows[i]) for i in sorted(rows)]
 
 
 # library kernel -> (benchmark stage, source files it is built from)
@@ -92,6 +109,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("dir", nargs="?")
     ap.add_argument("--copy-bytes", type=float, default=None)
+    ap.add_argument("--dispatches", default=None, help="list every dispatch of the kernels matching this name")
     ap.add_argument("--traffic", default=None, help="workload name for traffic lines")
     ap.add_argument("--fetch")
     ap.add_argument("--write")
@@ -123,6 +141,12 @@ def main():
                         if mx > 0:
                             print("scale %s on %s: %.4f bytes per unit (max dispatch %.1f units for %.0f bytes)"
                                   % (c, short(k, 40), a.copy_bytes / mx, mx, a.copy_bytes))
+    if a.dispatches:
+        rows = dispatches(a.dir, a.dispatches)
+        names = sorted({c for _, _, v in rows for c in v})
+        print("%10s %-40s " % ("dispatch", "kernel") + " ".join("%16s" % n for n in names))
+        for i, k, v in rows:
+            print("%10d %-40s " % (i, short(k, 40)) + " ".join("%16.1f" % v.get(c, float("nan")) for c in names))
 
 
 if __name__ == "__main__":
