@@ -202,9 +202,7 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.ctr = cv.take<long long>(rn::C_N);
     d.derr = cv.take<unsigned>(1);
     d.f_codes = cv.take<unsigned long long>(mh * CW);
-    d.f_hhash = cv.take<unsigned long long>(mh);
-    d.f_words = cv.take<int>(mh * 3);
-    d.f_hcslot = cv.take<int>(mh);
+    d.f_hrec = cv.take<rn::HistRec>(mh);
     d.f_hstat = cv.take<int>(mh);
     d.f_hslot = cv.take<int>(mh);
     d.f_hptr = cv.take<unsigned long long>(mh);
@@ -213,7 +211,7 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.f_rowdst = cv.take<unsigned long long>(mh);
     d.f_hval = cv.take<float>(mh * LH);
     d.f_qkey = cv.take<int4>(mq);
-    d.f_qw1 = cv.take<int>(mq);
+    d.f_qwords = cv.take<int4>(mq);
     d.f_qrec = cv.take<rn::QRec>(mq);
     d.f_qcand = cv.take<int>(mq);
     d.f_part = cv.take<int4>((mq + 3) / 4);

@@ -60,13 +60,20 @@ struct ScEnt {
     int pad[3];
 };
 
-// What the scorer needs per query, written by the frame planner (32 B).
+// What the scorer needs per query beyond its words, written by the frame
+// planner (16 B); the words (f_qwords) come from the keys kernel.
 struct QRec {
-    u64 hptr;   // address of the history's top-layer h' (or the stored score bits on a hit)
-    int t;      // target word
+    u64 hptr;   // address of the history's top-layer h'
     int flags;  // bits 0-1 base status (COMPUTED / Q_DUP), QF_CAND, QF_PROBE; bits 6.. staging slot
     int hs;     // history-cache slot after the frame (-1: not cached)
-    int w1, w2, w3;   // w-1 and the key's context words (-1 where unused)
+};
+
+// What the frame planner reads per history, written by the keys kernel as
+// one 16-byte record.
+struct HistRec {
+    u64 hash;   // 64-bit key hash
+    int slot;   // history-cache slot found before the frame, or -1
+    int w1;     // GRU input word (clamped into [0, V))
 };
 
 // Independent decode sessions per context (one frame each per launch).
@@ -104,9 +111,7 @@ struct Dev {
     unsigned *derr;
     // per-frame history scratch
     u64 *f_codes;     // [max_hist][CW]
-    u64 *f_hhash;
-    int *f_words;     // [max_hist][3], ids clamped into [0, V)
-    int *f_hcslot;    // cache slot found before the frame, or -1
+    HistRec *f_hrec;  // key hash, cache slot before the frame, input word
     int *f_hstat, *f_hslot;
     u64 *f_hptr;      // device address of each history's h' (all layers)
     int *f_roww;      // GRU input word (w-1) of row r
@@ -115,7 +120,7 @@ struct Dev {
     float *f_hval;    // [max_hist][LH] h' of rows the cache did not admit
     // per-frame query scratch
     int4 *f_qkey;     // (history index, w-2, w-3, target) for exact key checks
-    int *f_qw1;       // w-1 of each query's history
+    int4 *f_qwords;   // (w-1, w-2, w-3, target) of each query, as the scorer reads them
     QRec *f_qrec;
     int *f_qcand;     // admission candidates (used when the cache is nearly full)
     int4 *f_part;     // per scoring block: (computed, duplicates, hits, admitted), folded later
@@ -143,9 +148,7 @@ __host__ __device__ __forceinline__ Dev session_view(const Dev &d0, int s) {
     d.ctr = shift_ptr(d.ctr, o);
     d.derr = shift_ptr(d.derr, o);
     d.f_codes = shift_ptr(d.f_codes, o);
-    d.f_hhash = shift_ptr(d.f_hhash, o);
-    d.f_words = shift_ptr(d.f_words, o);
-    d.f_hcslot = shift_ptr(d.f_hcslot, o);
+    d.f_hrec = shift_ptr(d.f_hrec, o);
     d.f_hstat = shift_ptr(d.f_hstat, o);
     d.f_hslot = shift_ptr(d.f_hslot, o);
     d.f_hptr = shift_ptr(d.f_hptr, o);
@@ -154,7 +157,7 @@ __host__ __device__ __forceinline__ Dev session_view(const Dev &d0, int s) {
     d.f_rowdst = shift_ptr(d.f_rowdst, o);
     d.f_hval = shift_ptr(d.f_hval, o);
     d.f_qkey = shift_ptr(d.f_qkey, o);
-    d.f_qw1 = shift_ptr(d.f_qw1, o);
+    d.f_qwords = shift_ptr(d.f_qwords, o);
     d.f_qrec = shift_ptr(d.f_qrec, o);
     d.f_qcand = shift_ptr(d.f_qcand, o);
     d.f_part = shift_ptr(d.f_part, o);

@@ -103,7 +103,7 @@ __device__ void query_key(const Dev &d, const FrameArgs &f, int q) {
         if (w[c] < 0 || w[c] >= d.V) w[c] = 0;
     }
     d.f_qkey[q] = make_int4(i, d.me_order >= 3 ? w[1] : -1, d.me_order >= 4 ? w[2] : -1, t);
-    d.f_qw1[q] = w[0];
+    d.f_qwords[q] = make_int4(w[0], d.me_order >= 3 ? w[1] : -1, d.me_order >= 4 ? w[2] : -1, t);
     if (qerr) atomicOr(d.derr, qerr);
 }
 
@@ -232,11 +232,11 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     }
     if (lane == 0) {
         if (err) atomicOr(d.derr, err);
-        d.f_words[i * 3] = w3[0];
-        d.f_words[i * 3 + 1] = w3[1];
-        d.f_words[i * 3 + 2] = w3[2];
-        d.f_hhash[i] = h;
-        d.f_hcslot[i] = hit;
+        HistRec hr;
+        hr.hash = h;
+        hr.slot = hit;
+        hr.w1 = w3[0];
+        d.f_hrec[i] = hr;
         if (f.h_hash) f.h_hash[i] = h;
     }
 }

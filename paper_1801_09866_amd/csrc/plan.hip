@@ -82,7 +82,7 @@ __device__ __forceinline__ Race race_layout(int s0, int &base) {
 }
 
 __device__ bool same_hist_key(const Dev &d, int a, int b) {
-    if (d.f_words[a * 3] != d.f_words[b * 3]) return false;
+    if (d.f_hrec[a].w1 != d.f_hrec[b].w1) return false;
     const u64 *ca = d.f_codes + (size_t)a * d.CW, *cb = d.f_codes + (size_t)b * d.CW;
     for (int w = 0; w < d.CW; w += 4) {   // four independent loads per side per step
         u64 x = 0;
@@ -196,19 +196,18 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
         const int i = min(tid + r * PT, hlast);   // clamped: no divergent loads
-        h_hash[r] = d.f_hhash[i];
-        h_slot[r] = d.f_hcslot[i];
-        h_w1[r] = d.f_words[i * 3];
+        const HistRec hr = d.f_hrec[i];   // one 16-byte load per history
+        h_hash[r] = hr.hash;
+        h_slot[r] = hr.slot;
+        h_w1[r] = hr.w1;
         h_hp[r] = f.hist_ptr ? f.hist_ptr[i] : 0;   // handles are checked where they are used
     }
     int4 qk[QR];
-    int qw1[QR];
     const int qlast = nq > 0 ? nq - 1 : 0;
 #pragma unroll
     for (int r = 0; r < QR; ++r) {   // clamped, unconditional: idle rounds all read one element
         const int q = min(tid + r * PT, qlast);
         qk[r] = d.f_qkey[q];
-        qw1[r] = d.f_qw1[q];
     }
 
     // ---------------- race tables (block-uniform sizes) ----------------
@@ -381,7 +380,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
             int found = is;
             for (int j0 = 0; j0 < is; j0 += 64) {
                 const int j = j0 + lane;
-                const bool eq = j < is && d.f_hhash[min(j, hlast)] == hs && same_hist_key(d, j, is);
+                const bool eq = j < is && d.f_hrec[min(j, hlast)].hash == hs && same_hist_key(d, j, is);
                 const u64 b = __ballot(eq);
                 if (b) {
                     found = j0 + __ffsll((unsigned long long)b) - 1;
@@ -560,13 +559,9 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
                 const float *base = loc >= 0 ? d.hc_val + (size_t)loc * d.LH : d.f_hval + (size_t)(-loc - 1) * d.LH;
                 QRec rec;
                 rec.hptr = (u64)(base + (size_t)(d.L - 1) * d.H);
-                rec.t = qk[r].w;
                 rec.flags = (rep < q ? RNNLM_Q_DUP : RNNLM_Q_COMPUTED) | (cand ? QF_CAND : 0) |
                             ((s_rep[i] >> 16) == RNNLM_HC_HIT ? QF_PROBE : 0) | (cand ? rank << 6 : 0);
                 rec.hs = s_hsa[i];
-                rec.w1 = qw1[r];
-                rec.w2 = qk[r].y;
-                rec.w3 = qk[r].z;
                 d.f_qrec[q] = rec;
                 if (f.q_rep) f.q_rep[q] = rep;
             }

@@ -37,13 +37,15 @@ template <bool BF16>
 __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, int q, int lane, bool near_cap,
                                             int *s_cnt) {
     const QRec rec = d.f_qrec[q];
-    const int t = rec.t;
+    const int4 key = ldg<int4>(d.f_qwords + q);   // (w-1, w-2, w-3, target)
+    const int w1 = key.x;
+    const int t = key.w;
     const bool probe = rec.flags & QF_PROBE;   // wave-uniform: one query per wave
     // Once the record is in, everything the query can need is loaded at
     // once: the LM cache's first probe record (for a cached history key), the
     // output row, the history row, the bias and the MaxEnt weights. A hit
     // wastes the row loads but saves the round trip a miss would wait for.
-    unsigned pos = (unsigned)(query_hash((u64)rec.hs, rec.w2, rec.w3, t) & d.si_mask);
+    unsigned pos = (unsigned)(query_hash((u64)rec.hs, key.y, key.z, t) & d.si_mask);
     ScEnt e = d.sc_tab[probe ? pos : 0];
     const float *h = reinterpret_cast<const float *>(rec.hptr);
     float acc = 0.0f;
@@ -94,13 +96,13 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
         }
     }
     float me = d.b_out[t];
-    for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, rec.w1, rec.w2, rec.w3, t, d.me_log2)];
+    for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)];
     bool hit = false;
     float s = 0.0f;
     if (probe) {
         for (unsigned k = 0; k <= d.si_mask; ++k) {
             if (e.hs < 0) break;
-            if (e.hs == rec.hs && e.w2 == rec.w2 && e.w3 == rec.w3 && e.t == t) { hit = true; s = e.val; break; }
+            if (e.hs == rec.hs && e.w2 == key.y && e.w3 == key.z && e.t == t) { hit = true; s = e.val; break; }
             pos = (pos + 1) & d.si_mask;
             e = d.sc_tab[pos];
         }
@@ -115,7 +117,7 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
         if (near_cap) {
             d.f_qcand[q] = cand ? 1 : 0;
         } else if (rec.flags & QF_CAND) {   // own staging slot: entry, or unused on a hit
-            stage_score(d, rec.flags >> 6, cand ? rec.hs : -1, rec.w2, rec.w3, t, s);
+            stage_score(d, rec.flags >> 6, cand ? rec.hs : -1, key.y, key.z, t, s);
             if (cand) atomicAdd(&s_cnt[3], 1);
         }
     }
@@ -129,13 +131,13 @@ __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f,
             u64 *dst = d.hc_codes + (size_t)slot * d.CW;
             for (int w = lane; w < d.CW; w += 64) dst[w] = src[w];
             if (lane == 0) {
-                const u64 h = d.f_hhash[i];
+                const u64 h = d.f_hrec[i].hash;
                 unsigned pos = (unsigned)(h & d.hi_mask);
                 for (unsigned n = 0; n <= d.hi_mask; ++n) {
                     HcIdx *r = d.hc_idx + pos;
                     if (atomicCAS(&r->slot, -1, slot) == -1) {
                         r->hash = h;
-                        r->word = d.f_words[i * 3];
+                        r->word = d.f_hrec[i].w1;
                         break;
                     }
                     pos = (pos + 1) & d.hi_mask;
@@ -190,7 +192,8 @@ __device__ void admit_in_order(const Dev &d, const FrameArgs &f, int *s_tmp) {
         if (cand) {
             if (size0 + rank < d.cap_query) {
                 const QRec rec = d.f_qrec[q];
-                stage_score(d, rank, rec.hs, rec.w2, rec.w3, rec.t, f.scores[q]);
+                const int4 key = d.f_qwords[q];
+                stage_score(d, rank, rec.hs, key.y, key.z, key.w, f.scores[q]);
                 ++ins;
             } else {
                 ++rej;
