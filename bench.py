@@ -120,18 +120,20 @@ def algorithmic_work(cfg, st, qm, frames):
         else ("hbm", gru_bytes)
     orders = max(0, m.maxent_order - 1)
     computed = st["computed"] + st["query_dups"]
-    per_q = H * wb + 4 + 4 * orders + 8 + 4          # row, bias, MaxEnt, ids, score
+    per_q = H * wb + 4 + 4 * orders + 32 + 4         # row, bias, MaxEnt, words + work record, score
     return {
         "gru_gemm": gru,
         # scores (row gathers, h' reads, MaxEnt) + h' copy-out + history-cache inserts
         "score_finish": ("hbm", computed * per_q + st["score_hits"] * 16 + st["hists"] * H * 4
                          + 2 * st["hists"] * LH * 4 + st["hist_inserted"] * cw_bytes),
-        # history vectors in, codes out, hashes, cache-hit code comparisons
-        "hist_key": ("hbm", st["hists"] * (LH * 4 + 12 + cw_bytes + 8) + st["hist_hits"] * cw_bytes),
-        # the plan: per history hash + cache slot in, status/rep/slot/h' address out; per query
-        # key + w-1 in, 32 B work record + rep out; per GRU row its source and destination
-        "frame_plan": ("hbm", st["hists"] * (8 + 4 + 1 + 4 + 4 + 8 + 1) + st["queries"] * (16 + 4 + 32 + 4)
-                       + st["gru_rows"] * (4 + 8)),
+        # history vectors and words in, codes and 16 B records out, cache-hit code comparisons;
+        # query ids in, planner key and scorer words out
+        "hist_key": ("hbm", st["hists"] * (LH * 4 + 12 + cw_bytes + 16) + st["hist_hits"] * cw_bytes
+                     + st["queries"] * (8 + 16 + 16)),
+        # the plan: per history its 16 B record in, status/slot/h' address out; per query its key
+        # in and a 16 B work record out; per GRU row its word, source and destination
+        "frame_plan": ("hbm", st["hists"] * (16 + 4 + 4 + 8) + st["queries"] * (16 + 16)
+                       + st["gru_rows"] * (4 + 8 + 8)),
     }
 
 
