@@ -505,16 +505,21 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
         count_lanes(&s_cnt[1], live && h_st[r] == RNNLM_H_DUP);
     }
     // a new key whose history is (or will be) cached may enter the LM-query
-    // cache; candidates are ranked in query order
+    // cache; candidates are ranked in query order. When the history cache
+    // has room for all of the frame's new keys, every history is cached.
+    const bool all_cached = hc_size + s_htot <= d.cap_hist;   // block-uniform
 #pragma unroll
     for (int r = 0; r < QR; ++r) {
         if (r >= RQ) break;   // block-uniform
         const int q = tid + r * PT;
         bool cand = false;
         if (q < nq && qrepv[r] == q) {
-            int hsa, loc, row;
-            place(qk[r].x, hsa, loc, row);
-            cand = hsa >= 0;
+            cand = true;
+            if (!all_cached) {
+                int hsa, loc, row;
+                place(qk[r].x, hsa, loc, row);
+                cand = hsa >= 0;
+            }
         }
         const u64 b = __ballot(cand);
         if ((tid & 63) == 0) s_qflag[q >> 6] = b;
