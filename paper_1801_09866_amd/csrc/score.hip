@@ -20,6 +20,7 @@
 namespace rn {
 
 constexpr int kRowSteps = kMaxLH / 256;   // 16-byte fp32 steps per lane over the longest row
+constexpr int kCodeSteps = kMaxCW / 64;   // code words per lane of the longest key
 
 // staging slot e receives a new LM-query cache entry (hs = -1: slot unused)
 __device__ __forceinline__ void stage_score(const Dev &d, long long e, int hs, int w2, int w3, int t, float s) {
@@ -124,37 +125,49 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
 }
 
 __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f, int i, int lane) {
-    if (d.f_hstat[i] == RNNLM_H_REP) {
-        const int slot = d.f_hslot[i];
-        if (slot >= 0) {
-            const u64 *src = d.f_codes + (size_t)i * d.CW;
-            u64 *dst = d.hc_codes + (size_t)slot * d.CW;
-            for (int w = lane; w < d.CW; w += 64) dst[w] = src[w];
-            if (lane == 0) {
-                const u64 h = d.f_hrec[i].hash;
-                unsigned pos = (unsigned)(h & d.hi_mask);
-                for (unsigned n = 0; n <= d.hi_mask; ++n) {
-                    HcIdx *r = d.hc_idx + pos;
-                    if (atomicCAS(&r->slot, -1, slot) == -1) {
-                        r->hash = h;
-                        r->word = d.f_hrec[i].w1;
-                        break;
-                    }
-                    pos = (pos + 1) & d.hi_mask;
+    // one round of loads: status, slot after the frame, where h' lives, and
+    // the key's codes (needed if the key enters the cache)
+    const int st = d.f_hstat[i];
+    const int slot = d.f_hslot[i];
+    const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
+    const bool enter = st == RNNLM_H_REP && slot >= 0;   // wave-uniform
+    u64 code[kCodeSteps];
+    if (enter) {
+#pragma unroll
+        for (int c = 0; c < kCodeSteps; ++c)
+            if (lane + 64 * c < d.CW) code[c] = d.f_codes[(size_t)i * d.CW + lane + 64 * c];
+    }
+    // then the h' row, in flight while an admitted key enters the index
+    float4 v[kRowSteps];
+    if (f.hnew) {
+#pragma unroll
+        for (int k = 0; k < kRowSteps; ++k)
+            if (lane + 64 * k < d.LH / 4) v[k] = ldg<float4>(src + lane + 64 * k);
+    }
+    if (enter) {
+        u64 *dst = d.hc_codes + (size_t)slot * d.CW;
+#pragma unroll
+        for (int c = 0; c < kCodeSteps; ++c)
+            if (lane + 64 * c < d.CW) dst[lane + 64 * c] = code[c];
+        if (lane == 0) {
+            const HistRec hr = d.f_hrec[i];
+            unsigned pos = (unsigned)(hr.hash & d.hi_mask);
+            for (unsigned n = 0; n <= d.hi_mask; ++n) {
+                HcIdx *r = d.hc_idx + pos;
+                if (atomicCAS(&r->slot, -1, slot) == -1) {
+                    r->hash = hr.hash;
+                    r->word = hr.w1;
+                    break;
                 }
+                pos = (pos + 1) & d.hi_mask;
             }
         }
     }
-    if (f.hnew) {   // the whole row in flight, then stored
-        const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
+    if (f.hnew) {
         float4 *dst = reinterpret_cast<float4 *>(f.hnew + (size_t)i * d.LH);
-        float4 v[kRowSteps];
 #pragma unroll
-        for (int st = 0; st < kRowSteps; ++st)
-            if (lane + 64 * st < d.LH / 4) v[st] = ldg<float4>(src + lane + 64 * st);
-#pragma unroll
-        for (int st = 0; st < kRowSteps; ++st)
-            if (lane + 64 * st < d.LH / 4) dst[lane + 64 * st] = v[st];
+        for (int k = 0; k < kRowSteps; ++k)
+            if (lane + 64 * k < d.LH / 4) dst[lane + 64 * k] = v[k];
     }
 }
 
