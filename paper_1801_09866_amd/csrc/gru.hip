@@ -417,7 +417,7 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
 }
 
 // ------------------------------- fp32 -------------------------------------
-constexpr int F_BK = 32;
+constexpr int F_BK = 64;   // K step: long enough to cover a memory round trip with MFMA work
 constexpr int F_LDA = F_BK + 4;   // padded LDS row (floats)
 
 __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
@@ -435,29 +435,36 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
     const int K = Kx + d.H;
     const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
 
-    // A loader: row tid/8, 4 consecutive k at (tid%8)*4
+    // A loader: row tid/8, 4 consecutive k at (tid%8)*4 and 32 further on
     const int a_row = tid >> 3, a_k = (tid & 7) * 4;
     const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
-    // B loader: rows (gate, unit) tid/8 and tid/8 + 64
+    // B loader: rows (gate, unit) tid/8 and tid/8 + 64, the same two k chunks
     const int b_k = (tid & 7) * 4;
     const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
     const float *bp0 = Wp + (size_t)((b_r0 / G_BJ) * d.H + j0 + (b_r0 % G_BJ)) * K + b_k;
     const float *bp1 = Wp + (size_t)((b_r1 / G_BJ) * d.H + j0 + (b_r1 % G_BJ)) * K + b_k;
     const bool has_b1 = b_r1 < 3 * G_BJ;
 
-    float4 ra, rb0, rb1;
-    auto load = [&](int k0) {
-        const int k = k0 + a_k;
-        if (!src.valid) ra = make_float4(0.f, 0.f, 0.f, 0.f);
-        else if (k < Kx) ra = ldg<float4>(reinterpret_cast<const float *>(src.x) + k);
-        else ra = ldg<float4>(src.h + (k - Kx));
-        rb0 = ldg<float4>(bp0 + k0);
-        if (has_b1) rb1 = ldg<float4>(bp1 + k0);
+    float4 ra[2], rb0[2], rb1[2];
+    auto load = [&](int k0) {   // a K step lies wholly in the input part or the history part
+        const bool xp = k0 < Kx;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int k = k0 + a_k + 32 * c;
+            if (!src.valid) ra[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+            else if (xp) ra[c] = ldg<float4>(reinterpret_cast<const float *>(src.x) + k);
+            else ra[c] = ldg<float4>(src.h + (k - Kx));
+            rb0[c] = ldg<float4>(bp0 + k0 + 32 * c);
+            if (has_b1) rb1[c] = ldg<float4>(bp1 + k0 + 32 * c);
+        }
     };
     auto store = [&](int buf) {
-        *reinterpret_cast<float4 *>(&As[buf][a_row][a_k]) = ra;
-        *reinterpret_cast<float4 *>(&Bs[buf][b_r0][b_k]) = rb0;
-        if (has_b1) *reinterpret_cast<float4 *>(&Bs[buf][b_r1][b_k]) = rb1;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            *reinterpret_cast<float4 *>(&As[buf][a_row][a_k + 32 * c]) = ra[c];
+            *reinterpret_cast<float4 *>(&Bs[buf][b_r0][b_k + 32 * c]) = rb0[c];
+            if (has_b1) *reinterpret_cast<float4 *>(&Bs[buf][b_r1][b_k + 32 * c]) = rb1[c];
+        }
     };
 
     f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
@@ -473,7 +480,7 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
         if (kt + 1 < nk) load((kt + 1) * F_BK);
         const bool xphase = kt * F_BK < Kx;
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
+        for (int hh = 0; hh < F_BK / 16; ++hh) {
             const float4 a = *reinterpret_cast<const float4 *>(&As[buf][rb * 16 + fr][hh * 16 + fk]);
             const float4 br = *reinterpret_cast<const float4 *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
             const float4 bz = *reinterpret_cast<const float4 *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 16 + fk]);

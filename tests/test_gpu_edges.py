@@ -75,6 +75,18 @@ def test_ragged_sizes_empty_and_maximal():
     assert st["frames"] == 7
 
 
+def test_planner_maximal_frame():
+    """The planner's largest frame (2048 histories, 8192 queries): query keys
+    not staged in LDS, the query race table at load 1/2, keys left after the
+    race tables, and many equal keys of both kinds."""
+    rng = np.random.default_rng(17)
+    b = Both(M, weights(M, rng), Q_SIGN, max_hist=2048, max_query=8192, cap_hist=1 << 13, cap_query=1 << 15)
+    for t in range(2):
+        vec, words, qh, qt = rand_frame(rng, M, 2048, 8192, dup_every=5)
+        qt = rng.integers(0, 40, 8192).astype(np.int32)   # few targets: many equal query keys
+        b.frame(vec, words, qh, qt, tag="max %d" % t)
+
+
 def test_repeat_frame_hits_with_identical_bits():
     rng = np.random.default_rng(1)
     b = Both(M, weights(M, rng), Q_SIGDIG, 2)
