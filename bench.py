@@ -54,6 +54,10 @@ def parse():
                     help="check config: normalise the full output (NCE + MaxEnt logits of every word)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--io-frames", type=int, default=400,
+                    help="frames of the per-frame latency and PCIe-inclusive legs (0: skip both)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="saturation sweep: the key and scoring kernels at 1..8 maximal frames per launch")
     return ap.parse_args()
 
 
@@ -140,8 +144,8 @@ def algorithmic_work(cfg, st, qm, frames):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(the design for sharding is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the scoring path here has no multi-GPU launch",
+              file=sys.stderr)
         sys.exit(2)
     import torch
 
@@ -153,6 +157,8 @@ def main():
         args.warmup = 5 if cfg.queries == 0 else 50
     if args.steps is None:
         args.steps = cfg.frames - args.warmup
+    if args.sweep:
+        return main_sweep(args, cfg)
     if cfg.queries == 0:
         return main_check(args, cfg)
     if args.sessions > 1:
@@ -256,6 +262,16 @@ def main():
                     "us_per_launch": e["us_per_launch"]}
         log("stages:", json.dumps(stages))
 
+    # ---- per-frame latency, and the rate with each frame's block over PCIe --
+    io = None
+    if args.io_frames > 0 and K > 1:
+        P = min(args.io_frames, K)
+        io = {"frames": P}
+        io.update(latency_leg(sc, run, W, P, stream))
+        io.update(pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev))
+        io["resident_queries_per_s_same_frames"] = io.pop("resident_rate")
+        log("io:", json.dumps(io))
+
     if args.copy_calibration:
         a = torch.empty(64 << 20, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -285,29 +301,186 @@ def main():
         "wall_ms": round(wall * 1e3, 3),
         "roofline": roofline,
         "stages": stages,
+        "frame_io": io,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def hip_runtime():
+    """The HIP runtime torch has loaded (same soname as the library's), for
+    copies and events on streams of our own."""
+    H = ctypes.CDLL("libamdhip64.so.7")
+    vp, P = ctypes.c_void_p, ctypes.POINTER
+    H.hipMemcpyAsync.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, vp]
+    H.hipEventCreateWithFlags.argtypes = [P(vp), ctypes.c_uint]
+    H.hipEventRecord.argtypes = [vp, vp]
+    H.hipEventDestroy.argtypes = [vp]
+    H.hipStreamWaitEvent.argtypes = [vp, vp, ctypes.c_uint]
+    H.hipStreamSynchronize.argtypes = [vp]
+    H.hipEventElapsedTime.argtypes = [P(ctypes.c_float), vp, vp]
+    return H
+
+
+def _hip_ok(rc, what):
+    if rc != 0:
+        raise RuntimeError("%s failed: hip error %d" % (what, rc))
+
+
+def latency_leg(sc, run, W, P, stream):
+    """Frames W .. W+P-1 one at a time, the host waiting for each: host-observed
+    latency from the launch call to the frame's results being complete."""
+    import torch
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    lat = []
+    for i in range(W, W + P):
+        t = time.perf_counter()
+        run(i, i + 1)
+        stream.synchronize()
+        lat.append(time.perf_counter() - t)
+    lat = np.array(lat) * 1e6
+    return {"latency_us_p50": round(float(np.percentile(lat, 50)), 2),
+            "latency_us_p99": round(float(np.percentile(lat, 99)), 2),
+            "latency_us_max": round(float(lat.max()), 2)}
+
+
+def pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev):
+    """Frames W .. W+P-1 with their inputs starting in pinned host memory, as
+    a decoder on the host would hand them over: per frame, one copy of the
+    frame's block (history vectors, words, query ids) into one of two device
+    slots on a copy stream, the frame scored on the compute stream once its
+    copy is done, and its scores copied back to pinned host memory. Copies of
+    frame i+1 overlap scoring of frame i. Returns the rate with transfers and
+    the resident rate on the same frames (inputs already in HBM)."""
+    import torch
+
+    from paper_1801_09866_amd import rnnlm as R
+    H = hip_runtime()
+    al = lambda n: (n + 255) // 256 * 256
+    nh = [int(ho[i + 1] - ho[i]) for i in range(W, W + P)]
+    nq = [int(qo[i + 1] - qo[i]) for i in range(W, W + P)]
+    lay = [(0, al(a * LH * 4), al(a * LH * 4) + al(a * 12), al(a * LH * 4) + al(a * 12) + al(b * 4))
+           for a, b in zip(nh, nq)]
+    size = [l[3] + al(b * 4) for l, b in zip(lay, nq)]
+    host_off = np.concatenate([[0], np.cumsum(size)]).astype(np.int64)
+    host = torch.empty(int(host_off[-1]), dtype=torch.uint8, pin_memory=True)
+    for j, i in enumerate(range(W, W + P)):
+        base = int(host_off[j])
+        o = lay[j]
+        for off, t in ((o[0], hv[int(ho[i]):int(ho[i + 1])]), (o[1], hw[int(ho[i]):int(ho[i + 1])]),
+                       (o[2], qh[int(qo[i]):int(qo[i + 1])]), (o[3], qt[int(qo[i]):int(qo[i + 1])])):
+            b = t.contiguous().view(torch.uint8).reshape(-1).cpu()
+            host[base + off: base + off + b.numel()].copy_(b)
+    host_scores = torch.empty(sum(nq), dtype=torch.float32, pin_memory=True)
+    slot_bytes = max(size)
+    slots = [torch.empty(slot_bytes, dtype=torch.uint8, device=dev) for _ in range(2)]
+    dscore = [torch.empty(max(nq), dtype=torch.float32, device=dev) for _ in range(2)]
+    dh = [torch.empty((max(nh), LH), dtype=torch.float32, device=dev) for _ in range(2)]
+    frames, outs = [], []
+    for j in range(P):
+        s, o = slots[j % 2].data_ptr(), lay[j]
+        frames.append(R.Frame(nh[j], nq[j], s + o[0], s + o[1], s + o[2], s + o[3], None))
+        outs.append(R.Out(dscore[j % 2].data_ptr(), dh[j % 2].data_ptr(), None, None, None, None, None))
+    comp = torch.cuda.current_stream()
+    cs = torch.cuda.Stream()
+    sp, cp = ctypes.c_void_p(comp.cuda_stream), ctypes.c_void_p(cs.cuda_stream)
+
+    def event(flags):
+        e = ctypes.c_void_p()
+        _hip_ok(H.hipEventCreateWithFlags(ctypes.byref(e), flags), "hipEventCreateWithFlags")
+        return e
+    copied = [event(2), event(2)]   # hipEventDisableTiming
+    done = [event(2), event(2)]
+    t0, t1 = event(0), event(0)
+    qoff = np.concatenate([[0], np.cumsum(nq)]).astype(np.int64)
+
+    def leg():
+        _hip_ok(H.hipEventRecord(t0, sp), "hipEventRecord")
+        _hip_ok(H.hipStreamWaitEvent(cp, t0, 0), "hipStreamWaitEvent")
+        for j in range(P):
+            k = j % 2
+            if j >= 2:   # slot k is free once frame j-2 has been scored
+                _hip_ok(H.hipStreamWaitEvent(cp, done[k], 0), "hipStreamWaitEvent")
+            _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(slots[k].data_ptr()),
+                                     ctypes.c_void_p(host.data_ptr() + int(host_off[j])), size[j], 1, cp),
+                    "hipMemcpyAsync")
+            _hip_ok(H.hipEventRecord(copied[k], cp), "hipEventRecord")
+            _hip_ok(H.hipStreamWaitEvent(sp, copied[k], 0), "hipStreamWaitEvent")
+            rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[j]), ctypes.byref(outs[j]), sp)
+            if rc:
+                raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
+            _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(host_scores.data_ptr() + int(qoff[j]) * 4),
+                                     ctypes.c_void_p(dscore[k].data_ptr()), nq[j] * 4, 2, sp), "hipMemcpyAsync")
+            _hip_ok(H.hipEventRecord(done[k], sp), "hipEventRecord")
+        _hip_ok(H.hipEventRecord(t1, sp), "hipEventRecord")
+        _hip_ok(H.hipStreamSynchronize(sp), "hipStreamSynchronize")
+        ms = ctypes.c_float()
+        _hip_ok(H.hipEventElapsedTime(ctypes.byref(ms), t0, t1), "hipEventElapsedTime")
+        return ms.value / 1e3
+
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    secs = leg()
+    torch.cuda.synchronize()
+    # the same frames with inputs resident, for the comparison
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(comp)
+    run(W, W + P)
+    e1.record(comp)
+    torch.cuda.synchronize()
+    rsecs = e0.elapsed_time(e1) / 1e3
+    # the link itself: one large copy from the same pinned buffer
+    big = min(int(host_off[-1]), 256 << 20)
+    dbig = torch.empty(big, dtype=torch.uint8, device=dev)
+    _hip_ok(H.hipEventRecord(t0, cp), "hipEventRecord")
+    _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(dbig.data_ptr()), ctypes.c_void_p(host.data_ptr()), big, 1, cp),
+            "hipMemcpyAsync")
+    _hip_ok(H.hipEventRecord(t1, cp), "hipEventRecord")
+    _hip_ok(H.hipStreamSynchronize(cp), "hipStreamSynchronize")
+    ms = ctypes.c_float()
+    _hip_ok(H.hipEventElapsedTime(ctypes.byref(ms), t0, t1), "hipEventElapsedTime")
+    for e in copied + done + [t0, t1]:
+        H.hipEventDestroy(e)
+    h2d = int(sum(size))
+    return {"pcie_queries_per_s": round(sum(nq) / secs, 1),
+            "pcie_h2d_bytes_per_frame": h2d // P,
+            "pcie_h2d_GBs": round(h2d / secs / 1e9, 2),
+            "pcie_h2d_GBs_one_copy_of_%d_MiB" % (big >> 20): round(big / (ms.value / 1e3) / 1e9, 2),
+            "resident_rate": round(sum(nq) / rsecs, 1)}
 
 
 def cpu_baseline(args, wl, qm, qk, sc, run, frames):
     import torch
     from threadpoolctl import threadpool_info
 
+    from threadpoolctl import threadpool_limits
+
     from oracle import Oracle
     cfg, m = wl.cfg, wl.cfg.model
-    o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
-               cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
-    t = time.perf_counter()
-    nq = S = 0
-    for fr in wl.frames:
-        o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
-        nq += fr.n_query
-        S += 1
-        if time.perf_counter() - t >= args.cpu_seconds:
-            break
-    secs = time.perf_counter() - t
+
+    def sample(budget):
+        o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
+                   cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
+        t = time.perf_counter()
+        nq = S = 0
+        for fr in wl.frames:
+            o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
+            nq += fr.n_query
+            S += 1
+            if time.perf_counter() - t >= budget:
+                break
+        return S, nq, time.perf_counter() - t
+
+    S, nq, secs = sample(args.cpu_seconds)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    with threadpool_limits(limits=1):   # the same oracle on one thread, over a shorter prefix
+        S1, nq1, secs1 = sample(args.cpu_seconds / 3)
     # the GPU on exactly the same frames (cold caches, frame 0 on)
     sc.reset()
     torch.cuda.synchronize()
@@ -321,7 +494,9 @@ def cpu_baseline(args, wl, qm, qk, sc, run, frames):
     return {"value": round(nq / secs, 1), "unit": "queries/s", "cores": int(threads), "kind": "oracle",
             "sample": "frames 0..%d of the same workload from empty caches (%d queries, %.1f s)"
                       % (S - 1, nq, secs),
-            "gpu_value_same_sample": round(nq / gsec, 1)}
+            "gpu_value_same_sample": round(nq / gsec, 1),
+            "value_1_thread": round(nq1 / secs1, 1),
+            "sample_1_thread": "frames 0..%d (%d queries, %.1f s)" % (S1 - 1, nq1, secs1)}
 
 
 METRIC_CHECK = "full-vocabulary log-normalisers/sec (GRU step + logsumexp over V), H=1024 V=200k; % of fp32 MFMA roofline"
@@ -566,6 +741,73 @@ def main_sessions(args, cfg):
         "stages": stages, "roofline": None, "cpu_baseline": None,
     }
     print(json.dumps(line), flush=True)
+
+
+def main_sweep(args, cfg):
+    """Saturation sweep. A frame is at most 2048 histories and 8192 queries
+    (the planner's one-block limits), so one frame's key and scoring launches
+    last a few microseconds and mostly show latency. Here S = 1, 2, 4, 8
+    independent sessions each bring one maximal frame to one set of launches
+    (up to 16,384 histories and 65,536 queries per launch), with fresh random
+    histories, uniform target words and empty caches, so that every query is
+    scored and every history key is new. Each point is the median of 5
+    launches; the value per stage is its algorithmic bytes (or FLOPs) over its
+    kernel time, against the HBM (or MFMA) peak. Prints one JSON line per
+    point."""
+    import torch
+
+    from paper_1801_09866_amd import rnnlm as R
+    from paper_1801_09866_amd.workload import make_weights
+
+    m = cfg.model
+    qm, qk = qmode_of(args.qmode, cfg)
+    S_max, n_h, n_q = 8, 2048, 8192
+    t0 = time.time()
+    w = make_weights(m, 99)
+    log("weights generated in %.1fs" % (time.time() - t0))
+    LH = m.L * m.H
+    dev = torch.device("cuda:0")
+    sc = R.Scorer(m, w, qm, qk, max_hist=n_h, max_query=n_q, cap_hist=1 << 14, cap_query=1 << 16,
+                  device="cuda:0", sessions=S_max)
+    del w
+    g = torch.Generator(device=dev)
+    g.manual_seed(180109866)
+    hv = torch.tanh(torch.randn((S_max, n_h, LH), generator=g, device=dev)) * 0.9
+    hw = torch.randint(1, m.V, (S_max, n_h, 3), generator=g, device=dev, dtype=torch.int32)
+    qh = torch.randint(0, n_h, (S_max, n_q), generator=g, device=dev, dtype=torch.int32)
+    qt = torch.randint(0, m.V, (S_max, n_q), generator=g, device=dev, dtype=torch.int32)
+    frames = [(hv[k], hw[k], qh[k], qt[k]) for k in range(S_max)]
+    outs = [sc.alloc_out(n_h, n_q, hnew=True, debug=False) for _ in range(S_max)]
+    mfma_peak = PEAK["bf16_mfma_TFs"] if m.wdtype == 1 else PEAK["fp32_mfma_TFs"]
+    for S in (1, 2, 4, 8):
+        reps = []
+        for r in range(6):
+            sc.reset()
+            sc.profile(R.STAGES[:4])
+            sc.score_frames(frames[:S], outs[:S], hnew=True, debug=False)
+            torch.cuda.synchronize()
+            prof = sc.profile_read()
+            st = sc.stats()
+            if r > 0:   # the first launch at each size is a warm-up
+                reps.append({k: v[0] for k, v in prof.items()})
+        sc.profile(())
+        work = algorithmic_work(cfg, st, qm, 1)
+        point = {"sweep": "saturation", "sessions": S, "histories_per_launch": st["hists"],
+                 "queries_per_launch": st["queries"], "computed": st["computed"], "gru_rows": st["gru_rows"],
+                 "qmode": qmode_name(qm, qk), "stages": {}}
+        for name in R.STAGES[:4]:
+            ms = float(np.median([rp[name] for rp in reps]))
+            bound, amount = work[name]
+            e = {"us": round(ms * 1e3, 2), "bound": bound}
+            if bound == "mfma":
+                ach = amount / (ms / 1e3) / 1e12
+                e.update(TFLOPs=round(ach, 2), frac=round(ach / mfma_peak, 4))
+            else:
+                ach = amount / (ms / 1e3) / 1e9
+                e.update(MB=round(amount / 1e6, 2), GBs=round(ach, 1), frac=round(ach / PEAK["hbm_GBs"], 4))
+            point["stages"][name] = e
+        print(json.dumps(point), flush=True)
+    assert sc.stats()["device_error"] == 0
 
 
 if __name__ == "__main__":

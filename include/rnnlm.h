@@ -148,7 +148,10 @@ int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void *workspac
  * the histories and queries, run the GRU for uncached history keys, score the
  * uncached queries, fill `out`, then admit the frame's new keys to the caches
  * in ascending index while capacity lasts (a query's score is only admitted
- * when its history key is cached). Asynchronous on `stream`. */
+ * when its history key is cached). Asynchronous on `stream`. Only this call's
+ * kernels read the frame's inputs (and, through hist_ptr, the rows it names):
+ * once they have completed in stream order, the caller may reuse those
+ * buffers, e.g. as the target of the next frame's host-to-device copy. */
 int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *frame, const rnnlm_out *out, void *stream);
 
 /* A block of independent frames in one set of launches (Sec. 4 batches a

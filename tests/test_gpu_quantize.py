@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 import torch
 
+from harness import log
 from oracle import Q_EXACT, Q_SIGDIG, Q_SIGN, code_words, quantize
 from paper_1801_09866_amd import rnnlm as R
 
@@ -72,11 +73,31 @@ def test_sigdig_strided_sweep_all_bit_patterns(k):
 @pytest.mark.skipif(os.environ.get("RNNLM_EXHAUSTIVE") != "1", reason="set RNNLM_EXHAUSTIVE=1")
 @pytest.mark.parametrize("k", [1, 2, 3])
 def test_sigdig_exhaustive(k):
+    """Every fp32 value in [-1, 1] (2 x 1,065,353,217 bit patterns)."""
     chunk = 1 << 24
-    for lo in range(0, 0x3F800001, chunk):
+    for n, lo in enumerate(range(0, 0x3F800001, chunk)):
         bits = np.arange(lo, min(lo + chunk, 0x3F800001), dtype=np.uint32)
         x = bits.view(np.float32)
         check_sigdig(np.concatenate([x, -x]), k)
+        if n % 16 == 15:
+            log("  k=%d: bit patterns below %#x agree" % (k, lo + chunk))
+
+
+@pytest.mark.skipif(os.environ.get("RNNLM_EXHAUSTIVE") != "1", reason="set RNNLM_EXHAUSTIVE=1")
+def test_sign_exhaustive():
+    """Sign codes of every fp32 bit pattern (NaNs and infinities excluded,
+    since they raise the device flag)."""
+    chunk = 1 << 26
+    for lo in range(0, 1 << 32, chunk):
+        bits = np.arange(lo, lo + chunk, dtype=np.uint64).astype(np.uint32)
+        x = bits.view(np.float32)
+        x = x[np.isfinite(x)]
+        x = x[: len(x) // 64 * 64]
+        got, err = gpu_codes(x, Q_SIGN)
+        want = code_words(quantize(x.reshape(1, -1), Q_SIGN), Q_SIGN)[0]
+        assert np.array_equal(got.view(np.uint64)[: len(want)], want) and err == 0, hex(lo)
+        if (lo // chunk) % 16 == 15:
+            log("  sign: bit patterns below %#x agree" % (lo + chunk))
 
 
 def test_sigdig_flags_out_of_domain():

@@ -113,3 +113,59 @@ def test_a_device_error_in_one_session_is_sticky_for_the_context():
     g.reset()
     g.score_frames([good, good])
     assert g.stats()["device_error"] == 0
+
+
+def test_eight_sessions_of_maximal_frames():
+    """The largest launch the API allows: 8 sessions, each frame at the
+    planner's maxima (2048 histories, 8192 queries), with uniform targets and
+    a second block that repeats half of each session's histories and many of
+    its queries (cache hits). Every session must equal a context of its own,
+    and one session the oracle."""
+    rng = np.random.default_rng(88)
+    w = weights(M, rng)
+    S, n_h, n_q = 8, 2048, 8192
+    caps = (1 << 14, 1 << 16)
+    kw = dict(max_hist=n_h, max_query=n_q, cap_hist=caps[0], cap_query=caps[1])
+    multi = R.Scorer(M, w, Q_SIGN, 0, sessions=S, **kw)
+    solo = R.Scorer(M, w, Q_SIGN, 0, **kw)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    blocks = []
+    for t in range(2):
+        frs = []
+        for k in range(S):
+            vec = (np.tanh(rng.standard_normal((n_h, M.L * M.H))) * 0.9).astype(np.float32)
+            words = rng.integers(0, M.V, (n_h, 3)).astype(np.int32)
+            qh = rng.integers(0, n_h, n_q).astype(np.int32)
+            qt = rng.integers(0, M.V, n_q).astype(np.int32)
+            if t == 1:   # the previous frame's first half of histories, and their queries, again
+                pv, pw, pqh, pqt = blocks[0][k]
+                vec[: n_h // 2], words[: n_h // 2] = pv[: n_h // 2], pw[: n_h // 2]
+                sel = np.nonzero(pqh < n_h // 2)[0][: n_q // 2]
+                qh[: len(sel)], qt[: len(sel)] = pqh[sel], pqt[sel]
+            frs.append((vec, words, qh, qt))
+        blocks.append(frs)
+        log("  block", t, "of", S, "maximal frames")
+        outs = multi.score_frames([tuple(d(a) for a in fr) for fr in frs])
+        for k in range(S):
+            solo.reset()
+            for u in range(t + 1):
+                o1 = solo.score_frame(*(d(a) for a in blocks[u][k]))
+            torch.cuda.synchronize()
+            for key in KEYS:
+                a, b = outs[k][key], o1[key]
+                if key in ("scores", "hnew"):
+                    assert close(a.cpu().numpy(), b.cpu().numpy(), ATOL, RTOL)[0], (t, k, key)
+                else:
+                    assert torch.equal(a, b), (t, k, key)
+            if t == 1:
+                assert (outs[k]["q_status"] == R.Q_SCORE_HIT).sum().item() > n_q // 4, k
+    assert multi.stats()["device_error"] == 0
+    o = Oracle(M.V, M.E, M.H, M.L, M.maxent_log2, M.maxent_order, w, Q_SIGN, 0,
+               cap_hist=caps[0], cap_query=caps[1], seed=R.DEFAULT_SEED)
+    o.score_frame(*blocks[0][3])
+    res = o.score_frame(*blocks[1][3])
+    for key, want in (("q_status", res.q_status), ("q_rep", res.q_rep), ("h_status", res.h_status),
+                      ("h_rep", res.h_rep)):
+        assert np.array_equal(outs[3][key].cpu().numpy(), want), key
+    assert close(outs[3]["scores"].cpu().numpy(), res.scores, ATOL, RTOL)[0]
+    assert close(outs[3]["hnew"].cpu().numpy(), res.hnew, ATOL, RTOL)[0]
