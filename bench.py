@@ -349,11 +349,13 @@ def latency_leg(sc, run, W, P, stream):
 def pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev):
     """Frames W .. W+P-1 with their inputs starting in pinned host memory, as
     a decoder on the host would hand them over: per frame, one copy of the
-    frame's block (history vectors, words, query ids) into one of two device
-    slots on a copy stream, the frame scored on the compute stream once its
-    copy is done, and its scores copied back to pinned host memory. Copies of
-    frame i+1 overlap scoring of frame i. Returns the rate with transfers and
-    the resident rate on the same frames (inputs already in HBM)."""
+    frame's block (history vectors, words, query ids) into device memory, the
+    frame scored, and its scores copied back to pinned host memory, all in
+    stream order on the library's stream. (Copies on a second stream, ordered
+    by events, per frame or per 8 frames, measured no faster here: the copies
+    and the frame's kernels did not overlap.) Returns the rate with transfers,
+    the rate of one large copy from the same pinned buffer, and the resident
+    rate on the same frames (inputs already in HBM)."""
     import torch
 
     from paper_1801_09866_amd import rnnlm as R
@@ -373,48 +375,24 @@ def pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev):
                        (o[2], qh[int(qo[i]):int(qo[i + 1])]), (o[3], qt[int(qo[i]):int(qo[i + 1])])):
             b = t.contiguous().view(torch.uint8).reshape(-1).cpu()
             host[base + off: base + off + b.numel()].copy_(b)
-    host_scores = torch.empty(sum(nq), dtype=torch.float32, pin_memory=True)
-    slot_bytes = max(size)
-    slots = [torch.empty(slot_bytes, dtype=torch.uint8, device=dev) for _ in range(2)]
-    dscore = [torch.empty(max(nq), dtype=torch.float32, device=dev) for _ in range(2)]
-    dh = [torch.empty((max(nh), LH), dtype=torch.float32, device=dev) for _ in range(2)]
-    frames, outs = [], []
-    for j in range(P):
-        s, o = slots[j % 2].data_ptr(), lay[j]
-        frames.append(R.Frame(nh[j], nq[j], s + o[0], s + o[1], s + o[2], s + o[3], None))
-        outs.append(R.Out(dscore[j % 2].data_ptr(), dh[j % 2].data_ptr(), None, None, None, None, None))
-    comp = torch.cuda.current_stream()
-    cs = torch.cuda.Stream()
-    sp, cp = ctypes.c_void_p(comp.cuda_stream), ctypes.c_void_p(cs.cuda_stream)
-
-    def event(flags):
-        e = ctypes.c_void_p()
-        _hip_ok(H.hipEventCreateWithFlags(ctypes.byref(e), flags), "hipEventCreateWithFlags")
-        return e
-    copied = [event(2), event(2)]   # hipEventDisableTiming
-    done = [event(2), event(2)]
-    t0, t1 = event(0), event(0)
     qoff = np.concatenate([[0], np.cumsum(nq)]).astype(np.int64)
+    host_scores = torch.empty(int(qoff[-1]), dtype=torch.float32, pin_memory=True)
+    slot = torch.empty(max(size), dtype=torch.uint8, device=dev)
+    dscore = torch.empty(max(nq), dtype=torch.float32, device=dev)
+    dh = torch.empty((max(nh), LH), dtype=torch.float32, device=dev)
+    frames = [R.Frame(nh[j], nq[j], slot.data_ptr() + lay[j][0], slot.data_ptr() + lay[j][1],
+                      slot.data_ptr() + lay[j][2], slot.data_ptr() + lay[j][3], None) for j in range(P)]
+    out = R.Out(dscore.data_ptr(), dh.data_ptr(), None, None, None, None, None)
+    comp = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(comp.cuda_stream)
 
-    def leg():
-        _hip_ok(H.hipEventRecord(t0, sp), "hipEventRecord")
-        _hip_ok(H.hipStreamWaitEvent(cp, t0, 0), "hipStreamWaitEvent")
-        for j in range(P):
-            k = j % 2
-            if j >= 2:   # slot k is free once frame j-2 has been scored
-                _hip_ok(H.hipStreamWaitEvent(cp, done[k], 0), "hipStreamWaitEvent")
-            _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(slots[k].data_ptr()),
-                                     ctypes.c_void_p(host.data_ptr() + int(host_off[j])), size[j], 1, cp),
-                    "hipMemcpyAsync")
-            _hip_ok(H.hipEventRecord(copied[k], cp), "hipEventRecord")
-            _hip_ok(H.hipStreamWaitEvent(sp, copied[k], 0), "hipStreamWaitEvent")
-            rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[j]), ctypes.byref(outs[j]), sp)
-            if rc:
-                raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
-            _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(host_scores.data_ptr() + int(qoff[j]) * 4),
-                                     ctypes.c_void_p(dscore[k].data_ptr()), nq[j] * 4, 2, sp), "hipMemcpyAsync")
-            _hip_ok(H.hipEventRecord(done[k], sp), "hipEventRecord")
-        _hip_ok(H.hipEventRecord(t1, sp), "hipEventRecord")
+    def event():
+        e = ctypes.c_void_p()
+        _hip_ok(H.hipEventCreateWithFlags(ctypes.byref(e), 0), "hipEventCreateWithFlags")
+        return e
+    t0, t1 = event(), event()
+
+    def elapsed():
         _hip_ok(H.hipStreamSynchronize(sp), "hipStreamSynchronize")
         ms = ctypes.c_float()
         _hip_ok(H.hipEventElapsedTime(ctypes.byref(ms), t0, t1), "hipEventElapsedTime")
@@ -423,8 +401,25 @@ def pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev):
     sc.reset()
     run(0, W)
     torch.cuda.synchronize()
-    secs = leg()
-    torch.cuda.synchronize()
+    _hip_ok(H.hipEventRecord(t0, sp), "hipEventRecord")
+    for j in range(P):
+        _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(slot.data_ptr()), ctypes.c_void_p(host.data_ptr() + int(host_off[j])),
+                                 size[j], 1, sp), "hipMemcpyAsync")
+        rc = L.rnnlm_score_frame(ctx, ctypes.byref(frames[j]), ctypes.byref(out), sp)
+        if rc:
+            raise R.RnnlmError(rc, L.rnnlm_last_error().decode())
+        _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(host_scores.data_ptr() + int(qoff[j]) * 4),
+                                 ctypes.c_void_p(dscore.data_ptr()), nq[j] * 4, 2, sp), "hipMemcpyAsync")
+    _hip_ok(H.hipEventRecord(t1, sp), "hipEventRecord")
+    secs = elapsed()
+    # the link itself: one large copy from the same pinned buffer
+    big = min(int(host_off[-1]), 256 << 20)
+    dbig = torch.empty(big, dtype=torch.uint8, device=dev)
+    _hip_ok(H.hipEventRecord(t0, sp), "hipEventRecord")
+    _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(dbig.data_ptr()), ctypes.c_void_p(host.data_ptr()), big, 1, sp),
+            "hipMemcpyAsync")
+    _hip_ok(H.hipEventRecord(t1, sp), "hipEventRecord")
+    big_secs = elapsed()
     # the same frames with inputs resident, for the comparison
     sc.reset()
     run(0, W)
@@ -435,23 +430,13 @@ def pcie_leg(sc, L, ctx, run, W, P, hv, hw, qh, qt, ho, qo, LH, dev):
     e1.record(comp)
     torch.cuda.synchronize()
     rsecs = e0.elapsed_time(e1) / 1e3
-    # the link itself: one large copy from the same pinned buffer
-    big = min(int(host_off[-1]), 256 << 20)
-    dbig = torch.empty(big, dtype=torch.uint8, device=dev)
-    _hip_ok(H.hipEventRecord(t0, cp), "hipEventRecord")
-    _hip_ok(H.hipMemcpyAsync(ctypes.c_void_p(dbig.data_ptr()), ctypes.c_void_p(host.data_ptr()), big, 1, cp),
-            "hipMemcpyAsync")
-    _hip_ok(H.hipEventRecord(t1, cp), "hipEventRecord")
-    _hip_ok(H.hipStreamSynchronize(cp), "hipStreamSynchronize")
-    ms = ctypes.c_float()
-    _hip_ok(H.hipEventElapsedTime(ctypes.byref(ms), t0, t1), "hipEventElapsedTime")
-    for e in copied + done + [t0, t1]:
+    for e in (t0, t1):
         H.hipEventDestroy(e)
     h2d = int(sum(size))
     return {"pcie_queries_per_s": round(sum(nq) / secs, 1),
             "pcie_h2d_bytes_per_frame": h2d // P,
             "pcie_h2d_GBs": round(h2d / secs / 1e9, 2),
-            "pcie_h2d_GBs_one_copy_of_%d_MiB" % (big >> 20): round(big / (ms.value / 1e3) / 1e9, 2),
+            "pcie_h2d_GBs_one_copy_of_%d_MiB" % (big >> 20): round(big / big_secs / 1e9, 2),
             "resident_rate": round(sum(nq) / rsecs, 1)}
 
 

@@ -62,20 +62,32 @@ struct SessList {
     int sess[kMaxSessions];
 };
 
-__device__ __forceinline__ Rows make_rows(const Dev &d, const SessList &sl) {
+// The planner's GRU row count of each of the launch's frames, issued as the
+// kernel's first loads (entries past the frame count load frame 0's and are
+// not used), so that waiting for them waits for nothing issued later.
+struct RowCounts {
+    long long c[kMaxSessions];
+};
+
+__device__ __forceinline__ RowCounts load_row_counts(const Dev &d, const SessList &sl) {
+    RowCounts rc;
+#pragma unroll
+    for (int e = 0; e < kMaxSessions; ++e) {
+        const int ee = e < sl.n ? e : 0;
+        rc.c[e] = ldg<long long>(shift_ptr(d.ctr, (long long)sl.sess[ee] * d.sess_stride) + C_FRAME_M);
+    }
+    return rc;
+}
+
+__device__ __forceinline__ Rows make_rows(const Dev &d, const SessList &sl, const RowCounts &rc) {
     Rows R;
     R.n = sl.n;
-    int cnt[kMaxSessions];
 #pragma unroll
-    for (int e = 0; e < kMaxSessions; ++e) {   // all counters in flight at once
-        const int ee = e < sl.n ? e : 0;
-        R.sofs[e] = (long long)sl.sess[ee] * d.sess_stride;
-        const long long c = shift_ptr(d.ctr, R.sofs[e])[C_FRAME_M];
-        cnt[e] = e < sl.n ? (int)c : 0;
-    }
+    for (int e = 0; e < kMaxSessions; ++e) R.sofs[e] = (long long)sl.sess[e < sl.n ? e : 0] * d.sess_stride;
     R.moff[0] = 0;
 #pragma unroll
-    for (int e = 0; e < kMaxSessions; ++e) R.moff[e + 1] = R.moff[e] + cnt[e];
+    for (int e = 0; e < kMaxSessions; ++e)
+        R.moff[e + 1] = R.moff[e] + (e < sl.n ? __builtin_amdgcn_readfirstlane((int)rc.c[e]) : 0);
     return R;
 }
 
@@ -305,9 +317,53 @@ __device__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float 
 // the K loop.
 constexpr int N_MAXROWS = 32;   // rows handled by the narrow path at most
 constexpr int N_TILES = N_MAXROWS / 16;
+template <bool BF16W>
+constexpr int n_pass() { return BF16W ? 8 : 12; }   // steps whose operands are loaded together
+
+// Operands of the narrow path that do not depend on the frame's row count.
+// The kernel issues these loads as it starts, so that they are in flight
+// while the planner's row count comes back: the epilogue biases and the row
+// lists of the launch's first frame for rows 0..31 (read at indices clamped to
+// the lists' length; used only when that frame is the launch's only one, and
+// an entry only once its row is known to be below the count). The operand
+// rows they point at are then one round trip from the kernel's start instead
+// of two.
+template <bool BF16W>
+struct NarrowPre {
+    float br, bz, bn;
+    u64 rowh[N_TILES], rowd[N_TILES];   // A rows: history source, destination (the layer below's h')
+    int roww[N_TILES];                  // A rows: input word (first layer)
+    u64 edst, ehsrc;                    // epilogue row: destination and history source
+};
 
 template <bool BF16W>
-__device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float *smem, int g) {
+__device__ __forceinline__ void narrow_preload(const Dev &d, const SessList &sl, int layer, int g,
+                                               NarrowPre<BF16W> &p) {
+    const int tid = threadIdx.x, col = tid & 15;
+    // a fixed set of loads, none behind a branch
+    const int j = 4 * g + (tid & 3);
+    const float *bb = d.b_ih[layer];
+    p.br = ldg<float>(bb + j);
+    p.bz = ldg<float>(bb + d.H + j);
+    p.bn = ldg<float>(bb + 2 * d.H + j);
+    // the row lists of the launch's first frame (used when it is the only one)
+    const long long o = (long long)sl.sess[0] * d.sess_stride;
+    const int last = d.max_hist - 1;
+#pragma unroll
+    for (int t = 0; t < N_TILES; ++t) {
+        const int m = min(16 * t + col, last);
+        p.rowh[t] = ldg<u64>(shift_ptr(d.f_rowh, o) + m);
+        p.rowd[t] = ldg<u64>(shift_ptr(d.f_rowdst, o) + m);
+        p.roww[t] = ldg<int>(shift_ptr(d.f_roww, o) + m);
+    }
+    const int me = min(min(tid >> 2, N_MAXROWS - 1), last);
+    p.edst = ldg<u64>(shift_ptr(d.f_rowdst, o) + me);
+    p.ehsrc = ldg<u64>(shift_ptr(d.f_rowh, o) + me);
+}
+
+template <bool BF16W, bool USE_PRE, int NT>
+__device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float *smem, int g,
+                                           const NarrowPre<BF16W> &pre) {
     using T = typename MdOps<BF16W>::T;
     using E = typename std::conditional<BF16W, uint16_t, float>::type;
     constexpr int KS = BF16W ? 32 : 16;   // k per step
@@ -316,10 +372,13 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
     const int nsteps = K / KS;
     const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;   // scalars
     const int col = lane & 15, kq = (KS / 4) * (lane >> 4);
+    // columns 12..15 of the tile are padding: they repeat gate 0's weights, and
+    // the epilogue never reads them (an MFMA output column depends only on
+    // its own B column)
     const int gate = col >> 2, j0 = 4 * g;
-    const bool wcol = gate < 3;           // padding columns multiply zeros
-    const E *wrow = reinterpret_cast<const E *>(d.Wp[layer]) + (size_t)((wcol ? gate : 0) * d.H + j0 + (col & 3)) * K + kq;
+    const E *wrow = reinterpret_cast<const E *>(d.Wp[layer]) + (size_t)((gate < 3 ? gate : 0) * d.H + j0 + (col & 3)) * K + kq;
     const int nt = (M + 15) >> 4;         // row tiles (block-uniform)
+    const bool pre_rows = USE_PRE && R.n == 1;   // block-uniform
 
     // epilogue operands of thread (row m, unit u), loaded before the K loop
     const int em = tid >> 2, eu = tid & 3;
@@ -328,18 +387,48 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
     float *edst = nullptr;
     if (eth) {
         const int j = j0 + eu;
-        const float *bb = d.b_ih[layer];
-        ebr = bb[j];
-        ebz = bb[d.H + j];
-        ebn = bb[2 * d.H + j];
-        edst = reinterpret_cast<float *>(row_at(R, d.f_rowdst, em)) + (size_t)layer * d.H + j;
-        ehp = reinterpret_cast<const float *>(row_at(R, d.f_rowh, em))[(size_t)layer * d.H + j];
+        if (USE_PRE) {
+            ebr = pre.br;
+            ebz = pre.bz;
+            ebn = pre.bn;
+        } else {
+            const float *bb = d.b_ih[layer];
+            ebr = bb[j];
+            ebz = bb[d.H + j];
+            ebn = bb[2 * d.H + j];
+        }
+        const u64 dp = pre_rows ? pre.edst : (u64)row_at(R, d.f_rowdst, em);
+        const u64 hp = pre_rows ? pre.ehsrc : (u64)row_at(R, d.f_rowh, em);
+        edst = reinterpret_cast<float *>(dp) + (size_t)layer * d.H + j;
+        ehp = reinterpret_cast<const float *>(hp)[(size_t)layer * d.H + j];
     }
-    constexpr int PASS = BF16W ? 8 : 12;  // steps whose operands are loaded together (a wave has 6 bf16 steps at K = 1536)
+    constexpr int PASS = n_pass<BF16W>();   // a wave has 6 bf16 steps at K = 1536
     T b[PASS];
-    RowSrc src[N_TILES];
+    RowSrc src[NT];
 #pragma unroll
-    for (int t = 0; t < N_TILES; ++t) src[t] = row_source(d, R, layer, 16 * t + col, M);
+    for (int t = 0; t < NT; ++t) {
+        const int m = 16 * t + col;
+        if (pre_rows) {
+            RowSrc &r = src[t];
+            r.valid = m < M;
+            r.x_bf16 = false;
+            r.x = nullptr;
+            r.h = nullptr;
+            if (r.valid) {
+                r.h = reinterpret_cast<const float *>(pre.rowh[t]) + (size_t)layer * d.H;
+                if (layer == 0) {
+                    const size_t wd = (size_t)(unsigned)pre.roww[t];
+                    r.x_bf16 = d.wdtype == RNNLM_BF16;
+                    r.x = r.x_bf16 ? (const void *)(reinterpret_cast<const uint16_t *>(d.emb) + wd * d.E)
+                                   : (const void *)(reinterpret_cast<const float *>(d.emb) + wd * d.E);
+                } else {
+                    r.x = reinterpret_cast<const float *>(pre.rowd[t]) + (size_t)(layer - 1) * d.H;
+                }
+            }
+        } else {
+            src[t] = row_source(d, R, layer, m, M);
+        }
+    }
 
     auto loadA = [&](const RowSrc &rs, int k) -> T {
         if (!rs.valid) return T{0, 0, 0, 0};
@@ -353,19 +442,19 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
         return __builtin_bit_cast(T, pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4)));
     };
 
-    f4_t accx[N_TILES], acch[N_TILES];
+    f4_t accx[NT], acch[NT];
 #pragma unroll
-    for (int t = 0; t < N_TILES; ++t) accx[t] = acch[t] = f4_t{0, 0, 0, 0};
+    for (int t = 0; t < NT; ++t) accx[t] = acch[t] = f4_t{0, 0, 0, 0};
     for (int p0 = s0; p0 < s1; p0 += PASS) {
-        T a[N_TILES][PASS];
+        T a[NT][PASS];
 #pragma unroll
         for (int c = 0; c < PASS; ++c) {
             const int st = p0 + c;
             if (st < s1) {   // wave-uniform
                 const int k = st * KS;
-                b[c] = wcol ? ldg<T>(wrow + k) : T{0, 0, 0, 0};
+                b[c] = ldg<T>(wrow + k);
 #pragma unroll
-                for (int t = 0; t < N_TILES; ++t)
+                for (int t = 0; t < NT; ++t)
                     if (t < nt) a[t][c] = loadA(src[t], k + kq);
             }
         }
@@ -375,7 +464,7 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
             if (st < s1) {
                 const bool xp = st * KS < Kx;   // wave-uniform
 #pragma unroll
-                for (int t = 0; t < N_TILES; ++t) {
+                for (int t = 0; t < NT; ++t) {
                     if (t < nt) {
                         if (xp) accx[t] = md_mfma(a[t][c], b[c], accx[t]);
                         else acch[t] = md_mfma(a[t][c], b[c], acch[t]);
@@ -386,10 +475,10 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
     }
     // partial tiles to LDS: [wave][tile][part][lane][4]
 #pragma unroll
-    for (int t = 0; t < N_TILES; ++t) {
+    for (int t = 0; t < NT; ++t) {
         if (t < nt) {
-            float *px = smem + ((size_t)((w * N_TILES + t) * 2 + 0) * 64 + lane) * 4;
-            float *ph = smem + ((size_t)((w * N_TILES + t) * 2 + 1) * 64 + lane) * 4;
+            float *px = smem + ((size_t)((w * NT + t) * 2 + 0) * 64 + lane) * 4;
+            float *ph = smem + ((size_t)((w * NT + t) * 2 + 1) * 64 + lane) * 4;
             *reinterpret_cast<float4 *>(px) = make_float4(accx[t][0], accx[t][1], accx[t][2], accx[t][3]);
             *reinterpret_cast<float4 *>(ph) = make_float4(acch[t][0], acch[t][1], acch[t][2], acch[t][3]);
         }
@@ -400,8 +489,8 @@ __device__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float 
         const int t = em >> 4, i = em & 15, e = i & 3, lb = 16 * (i >> 2);
         float xr = 0.f, xz = 0.f, xn = 0.f, hr = 0.f, hz = 0.f, hn = 0.f;
         for (int v = 0; v < 8; ++v) {   // fixed order: equal inputs give equal bits
-            const float *px = smem + (size_t)((v * N_TILES + t) * 2 + 0) * 256 + e;
-            const float *ph = smem + (size_t)((v * N_TILES + t) * 2 + 1) * 256 + e;
+            const float *px = smem + (size_t)((v * NT + t) * 2 + 0) * 256 + e;
+            const float *ph = smem + (size_t)((v * NT + t) * 2 + 1) * 256 + e;
             xr += px[(lb + eu) * 4];
             xz += px[(lb + 4 + eu) * 4];
             xn += px[(lb + 8 + eu) * 4];
@@ -600,18 +689,52 @@ static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles excee
 static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
 static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
-template <bool BF16W>
+// ONE: the launch scores a single frame (the host knows), so the row lists
+// need no per-frame selection and the narrow path's operands can be loaded
+// before the row count is known.
+template <bool BF16W, bool ONE>
 __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer) {
     __shared__ __align__(16) float smem[G_LDS_FLOATS];
-    const Rows R = make_rows(d, sl);
+    // the narrow path's unit group of a block index: each XCD its own contiguous share
+    const int NB = d.H / 4;
+    const bool by_xcd = ((NB & 7) == 0) & ((int)gridDim.x >= NB);   // no branch: a select
+    auto group = [&](int t) { return by_xcd ? (t & 7) * (NB >> 3) + (t >> 3) : t; };
+    NarrowPre<BF16W> pre;
+    Rows R;
+    if (ONE) {
+        // every block loads one group's operands (a block past the groups the last one's, unused)
+        narrow_preload<BF16W>(d, sl, layer, min(group(blockIdx.x), NB - 1), pre);
+        const long long c = ldg<long long>(shift_ptr(d.ctr, (long long)sl.sess[0] * d.sess_stride) + C_FRAME_M);
+        // The row count takes a dependence on the preloaded values, times a
+        // zero the compiler cannot see (a launch of one frame has sl.n = 1).
+        // Without a use ahead of the branch on the count, the compiler moves
+        // these loads into the narrow path, behind the count's round trip;
+        // with it, the count and the operands arrive in the same round trip.
+        const u64 mix = pre.rowh[0] ^ pre.rowd[0] ^ pre.edst ^ pre.ehsrc ^ (u64)(unsigned)pre.roww[0] ^
+                        (u64)(__float_as_uint(pre.br) ^ __float_as_uint(pre.bz) ^ __float_as_uint(pre.bn));
+        const int dep = __builtin_amdgcn_readfirstlane((int)(mix ^ (mix >> 32))) * (sl.n - 1);
+        R.n = 1;
+        R.sofs[0] = (long long)sl.sess[0] * d.sess_stride;
+#pragma unroll
+        for (int e = 1; e < kMaxSessions; ++e) R.sofs[e] = R.sofs[0];
+        R.moff[0] = 0;
+#pragma unroll
+        for (int e = 1; e <= kMaxSessions; ++e) R.moff[e] = (int)c + dep;
+    } else {
+        R = make_rows(d, sl, load_row_counts(d, sl));
+    }
     const int M = R.moff[kMaxSessions];   // rows of all the launch's frames
     if (M <= 0) return;
-    if (M <= N_MAXROWS) {             // few rows: every CU streams its share of the weights
-        const int NB = d.H / 4;
-        for (int t = blockIdx.x; t < NB; t += gridDim.x) {
-            const int g = (NB & 7) == 0 && (int)gridDim.x >= NB ? (t & 7) * (NB >> 3) + (t >> 3) : t;
+    if (ONE && M <= 16) {             // few rows: every CU streams its share of the weights
+        if ((int)blockIdx.x < NB) gru_narrow<BF16W, true, 1>(d, R, layer, M, smem, group(blockIdx.x), pre);
+        for (int t = blockIdx.x + gridDim.x; t < NB; t += gridDim.x) {
             __syncthreads();
-            gru_narrow<BF16W>(d, R, layer, M, smem, g);
+            gru_narrow<BF16W, false, 1>(d, R, layer, M, smem, group(t), pre);
+        }
+    } else if (M <= N_MAXROWS) {      // the same, one or two row tiles
+        for (int t = blockIdx.x; t < NB; t += gridDim.x) {
+            __syncthreads();
+            gru_narrow<BF16W, false, N_TILES>(d, R, layer, M, smem, group(t), pre);
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
         gru_medium<BF16W>(d, R, layer, M, smem);
@@ -659,10 +782,13 @@ void launch_gru_layer(const Dev &d, const FrameBlock &fb, int layer, int max_row
     for (int e = 0; e < kMaxSessions; ++e) sl.sess[e] = e < fb.n ? fb.sess[e] : 0;
     // one block per CU (the LDS buffer allows no more); blocks loop over tiles
     const int blocks = 256;
-    if (d.wdtype == RNNLM_BF16)
-        launch_k(k_gru<true>, blocks, G_THREADS, s, ts, d, sl, layer);
-    else
-        launch_k(k_gru<false>, blocks, G_THREADS, s, ts, d, sl, layer);
+    if (d.wdtype == RNNLM_BF16) {
+        if (fb.n == 1) launch_k(k_gru<true, true>, blocks, G_THREADS, s, ts, d, sl, layer);
+        else launch_k(k_gru<true, false>, blocks, G_THREADS, s, ts, d, sl, layer);
+    } else {
+        if (fb.n == 1) launch_k(k_gru<false, true>, blocks, G_THREADS, s, ts, d, sl, layer);
+        else launch_k(k_gru<false, false>, blocks, G_THREADS, s, ts, d, sl, layer);
+    }
 }
 
 }  // namespace rn
