@@ -524,9 +524,13 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
     const int K = Kx + d.H;
     const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
 
-    // A loader: row tid/8, 4 consecutive k at (tid%8)*4 and 32 further on
+    // A loader: row tid/8, 4 consecutive k at (tid%8)*4 and 32 further on.
+    // Rows past M load row M - 1 (m0 < M): their products only reach output
+    // rows the epilogue does not write, and no select sits between a load
+    // and its use.
     const int a_row = tid >> 3, a_k = (tid & 7) * 4;
-    const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
+    const RowSrc src = row_source(d, R, layer, min(m0 + a_row, M - 1), M);
+    const float *ax = reinterpret_cast<const float *>(src.x), *ah = src.h;
     // B loader: rows (gate, unit) tid/8 and tid/8 + 64, the same two k chunks
     const int b_k = (tid & 7) * 4;
     const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
@@ -534,67 +538,80 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
     const float *bp1 = Wp + (size_t)((b_r1 / G_BJ) * d.H + j0 + (b_r1 % G_BJ)) * K + b_k;
     const bool has_b1 = b_r1 < 3 * G_BJ;
 
-    float4 ra[2], rb0[2], rb1[2];
-    auto load = [&](int k0) {   // a K step lies wholly in the input part or the history part
-        const bool xp = k0 < Kx;
+    // Two register stages: the loads of K step s + 2 are issued while step s
+    // multiplies, so each has two steps of MFMA work to arrive in.
+    struct Stage {
+        float4 a[2], b0[2], b1[2];
+    };
+    auto load = [&](Stage &S, int k0) {   // a K step lies wholly in the input part or the history part
+        const float *ap = k0 < Kx ? ax + k0 : ah + (k0 - Kx);   // uniform choice
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-            const int k = k0 + a_k + 32 * c;
-            if (!src.valid) ra[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-            else if (xp) ra[c] = ldg<float4>(reinterpret_cast<const float *>(src.x) + k);
-            else ra[c] = ldg<float4>(src.h + (k - Kx));
-            rb0[c] = ldg<float4>(bp0 + k0 + 32 * c);
-            if (has_b1) rb1[c] = ldg<float4>(bp1 + k0 + 32 * c);
+            S.a[c] = ldg<float4>(ap + a_k + 32 * c);
+            S.b0[c] = ldg<float4>(bp0 + k0 + 32 * c);
+            if (has_b1) S.b1[c] = ldg<float4>(bp1 + k0 + 32 * c);
         }
     };
-    auto store = [&](int buf) {
+    auto store = [&](const Stage &S, int buf) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-            *reinterpret_cast<float4 *>(&As[buf][a_row][a_k + 32 * c]) = ra[c];
-            *reinterpret_cast<float4 *>(&Bs[buf][b_r0][b_k + 32 * c]) = rb0[c];
-            if (has_b1) *reinterpret_cast<float4 *>(&Bs[buf][b_r1][b_k + 32 * c]) = rb1[c];
+            *reinterpret_cast<float4 *>(&As[buf][a_row][a_k + 32 * c]) = S.a[c];
+            *reinterpret_cast<float4 *>(&Bs[buf][b_r0][b_k + 32 * c]) = S.b0[c];
+            if (has_b1) *reinterpret_cast<float4 *>(&Bs[buf][b_r1][b_k + 32 * c]) = S.b1[c];
         }
     };
 
     f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
     const int rb = w & 3, ub = w >> 2;
     const int fr = lane & 15, fk = 4 * (lane >> 4);
-
-    const int nk = K / F_BK;
-    load(0);
-    store(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load((kt + 1) * F_BK);
-        const bool xphase = kt * F_BK < Kx;
+    // a step's LDS fragments are all read before its MFMAs, so that their
+    // latency is paid once per step; the candidate gate's accumulator is
+    // chosen once per step (a step lies in one part of K)
+    auto compute = [&](int buf, bool xphase) {
+        float4 a[F_BK / 16], br[F_BK / 16], bz[F_BK / 16], bn[F_BK / 16];
 #pragma unroll
         for (int hh = 0; hh < F_BK / 16; ++hh) {
-            const float4 a = *reinterpret_cast<const float4 *>(&As[buf][rb * 16 + fr][hh * 16 + fk]);
-            const float4 br = *reinterpret_cast<const float4 *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-            const float4 bz = *reinterpret_cast<const float4 *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-            const float4 bn = *reinterpret_cast<const float4 *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-            const float av[4] = {a.x, a.y, a.z, a.w};
-            const float rv[4] = {br.x, br.y, br.z, br.w};
-            const float zv[4] = {bz.x, bz.y, bz.z, bz.w};
-            const float nv[4] = {bn.x, bn.y, bn.z, bn.w};
-            if (xphase) {
+            a[hh] = *reinterpret_cast<const float4 *>(&As[buf][rb * 16 + fr][hh * 16 + fk]);
+            br[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
+            bz[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
+            bn[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
+        }
+        f4_t an = xphase ? anx : anh;
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
-                    az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
-                    anx = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anx, 0, 0, 0);
-                }
-            } else {
+        for (int hh = 0; hh < F_BK / 16; ++hh) {
+            const float av[4] = {a[hh].x, a[hh].y, a[hh].z, a[hh].w};
+            const float rv[4] = {br[hh].x, br[hh].y, br[hh].z, br[hh].w};
+            const float zv[4] = {bz[hh].x, bz[hh].y, bz[hh].z, bz[hh].w};
+            const float nv[4] = {bn[hh].x, bn[hh].y, bn[hh].z, bn[hh].w};
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
-                    az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
-                    anh = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], anh, 0, 0, 0);
-                }
+            for (int c = 0; c < 4; ++c) {
+                ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
+                az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
+                an = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], an, 0, 0, 0);
             }
         }
-        if (kt + 1 < nk) store(buf ^ 1);
+        if (xphase) anx = an;
+        else anh = an;
+    };
+
+    // S0 carries the odd steps and S1 the even ones from step 2 on; LDS buffer
+    // s & 1 holds step s
+    const int nk = K / F_BK;   // >= 2: E, H are multiples of 64
+    Stage S0, S1;
+    load(S0, 0);
+    store(S0, 0);
+    load(S0, F_BK);
+    if (nk > 2) load(S1, 2 * F_BK);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+        compute(0, kt * F_BK < Kx);
+        if (kt + 1 < nk) store(S0, 1);
+        if (kt + 3 < nk) load(S0, (kt + 3) * F_BK);
+        __syncthreads();
+        if (kt + 1 >= nk) break;
+        compute(1, (kt + 1) * F_BK < Kx);
+        if (kt + 2 < nk) store(S1, 0);
+        if (kt + 4 < nk) load(S1, (kt + 4) * F_BK);
         __syncthreads();
     }
     gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
