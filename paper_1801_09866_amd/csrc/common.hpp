@@ -247,16 +247,6 @@ __device__ __forceinline__ T ldg(const void *p) {
     }
 }
 
-// Uniform load through the constant address space, which the compiler turns
-// into a scalar load (waited on by the LDS/scalar counter, so that waiting for
-// it does not also wait for vector loads in flight). Only for data that no
-// kernel writes while this one runs, such as counters an earlier kernel on the
-// stream produced: the scalar cache starts each kernel empty.
-template <typename T>
-__device__ __forceinline__ T sld(const T *p) {
-    return *reinterpret_cast<const __attribute__((address_space(4))) T *>(reinterpret_cast<uintptr_t>(p));
-}
-
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 __device__ __forceinline__ float wave_sum(float v) {
