@@ -16,6 +16,12 @@ The second form prints one line per library kernel,
 with the mean FETCH_SIZE and WRITE_SIZE per dispatch scaled to bytes, and a
 hash of the sources the kernel is built from, so that a reader (bench.py) can
 tell whether the kernel has changed since the counters were taken.
+
+    python -m paper_1801_09866_amd.profsum --sweep-trace DIR --fetch DIR --write DIR \
+        --mfma DIR --fetch-scale B --write-scale B [--group 6]
+
+The third form summarises bench.py --sweep: per library kernel and sweep
+size, mean duration, HBM bytes and MFMA utilisation per launch.
 """
 import argparse
 import collections
@@ -89,6 +95,61 @@ def stage_of(kernel_name):
     return KERNELS.get(base)
 
 
+def trace_dispatches(d):
+    """Kernel-trace rows: [(dispatch id, kernel, duration in ns)] in dispatch order."""
+    out = []
+    for p in glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True):
+        with open(p) as f:
+            for r in csv.DictReader(f):
+                out.append((int(r["Dispatch_Id"]), r["Kernel_Name"],
+                            int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    return sorted(out)
+
+
+def family(kernel_name):
+    return kernel_name.split("(")[0].replace("void ", "").split("<")[0].strip()
+
+
+def sweep(a):
+    """Saturation sweep: each library kernel family's dispatches in order,
+    in groups of `group` launches of one size (the first of each group is a
+    warm-up and left out): mean duration, HBM bytes (counter units times the
+    scales) and MFMA utilisation per launch."""
+    fam_of = lambda k: family(k) if stage_of(k) else None
+    dur = collections.defaultdict(list)
+    for _, k, ns in trace_dispatches(a.sweep_trace):
+        if fam_of(k):
+            dur[fam_of(k)].append(ns)
+    cnt = collections.defaultdict(lambda: collections.defaultdict(list))
+    for dd in (a.fetch, a.write, a.mfma):
+        if not dd:
+            continue
+        rows = collections.defaultdict(dict)
+        kern = {}
+        for p in glob.glob(os.path.join(dd, "**", "*counter_collection.csv"), recursive=True):
+            with open(p) as f:
+                for r in csv.DictReader(f):
+                    i = int(r["Dispatch_Id"])
+                    rows[i][r["Counter_Name"]] = rows[i].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                    kern[i] = r["Kernel_Name"]
+        for i in sorted(rows):
+            if fam_of(kern[i]):
+                for c, v in rows[i].items():
+                    cnt[fam_of(kern[i])][c].append(v)
+    g = a.group
+    print("%-22s %5s %10s %12s %12s %9s" % ("kernel", "size", "us", "fetch_MB", "write_MB", "MfmaUtil"))
+    for fam in sorted(dur):
+        n = len(dur[fam]) // g
+        for s in range(n):
+            sl = slice(s * g + 1, (s + 1) * g)
+            mean = lambda v: sum(v[sl]) / len(v[sl]) if len(v) >= (s + 1) * g else float("nan")
+            us = mean(dur[fam]) / 1e3
+            fb = mean(cnt[fam]["FETCH_SIZE"]) * a.fetch_scale / 1e6 if cnt[fam].get("FETCH_SIZE") else float("nan")
+            wb = mean(cnt[fam]["WRITE_SIZE"]) * a.write_scale / 1e6 if cnt[fam].get("WRITE_SIZE") else float("nan")
+            mu = mean(cnt[fam]["MfmaUtil"]) if cnt[fam].get("MfmaUtil") else float("nan")
+            print("%-22s %5d %10.2f %12.2f %12.2f %9.1f" % (fam, s, us, fb, wb, mu))
+
+
 def traffic(a):
     fetch, write = counters(a.fetch), counters(a.write)
     for k in sorted(set(fetch) | set(write)):
@@ -115,7 +176,12 @@ def main():
     ap.add_argument("--write")
     ap.add_argument("--fetch-scale", type=float, default=None)
     ap.add_argument("--write-scale", type=float, default=None)
+    ap.add_argument("--sweep-trace", default=None, help="saturation sweep: the kernel-trace run's directory")
+    ap.add_argument("--mfma", default=None, help="saturation sweep: an MfmaUtil counter run's directory")
+    ap.add_argument("--group", type=int, default=6, help="saturation sweep: launches per size")
     a = ap.parse_args()
+    if a.sweep_trace:
+        return sweep(a)
     if a.traffic:
         return traffic(a)
     ks = kernel_stats(a.dir)
