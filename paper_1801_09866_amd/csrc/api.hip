@@ -330,7 +330,8 @@ RNNLM_API int rnnlm_score_frames(rnnlm_t *ctx, const rnnlm_frame *frames, const 
         fb.f[e] = f;
         fb.sess[e] = k;
         fb.npart[e] = ctx->pending_parts[k];
-        fb.hoff[e + 1] = fb.hoff[e] + (f.n_hist + 3) / 4;
+        // key blocks: one per history for k significant digits, else one per 4 histories
+        fb.hoff[e + 1] = fb.hoff[e] + (c.qmode == RNNLM_Q_SIGDIG ? f.n_hist : (f.n_hist + 3) / 4);
         fb.qoff[e + 1] = fb.qoff[e] + (f.n_query + 255) / 256;
         fb.soff[e + 1] = fb.soff[e] + (ctx->staged_max[k] + 255) / 256;
         fb.qblk[e] = (f.n_query + 3) / 4;

@@ -241,6 +241,103 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     }
 }
 
+// SIGDIG: one block (4 waves) per history. The quantiser's integer work is
+// the kernel's cost in this mode, so thread t takes code words t and t + 256
+// (elements 4w..4w+3), four times as many lanes per history as one wave
+// would give it. The key hash is a wrapping sum, so the four waves' partial
+// sums combine in any order; the cache probe walks the same index records in
+// every wave, and a candidate's codes are compared by all four.
+constexpr int kSdWords = kMaxLH / 4 / 256;   // code words per thread of the longest vector
+
+__device__ void hist_block_sigdig(const Dev &d, const FrameArgs &f, const DecadeTab &T, int i) {
+    __shared__ u64 s_sum[4];
+    __shared__ int s_flag[4];
+    const int tid = threadIdx.x, lane = tid & 63, wv = wave_id();
+    if (i >= f.n_hist) return;   // block-uniform
+    int w3[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) w3[c] = f.hist_words[(size_t)i * 3 + c];
+    bool hbad = false;
+    const float *x = hist_row(d, f, i, hbad);
+    const int CW = d.CW;
+    float4 v[kSdWords];
+#pragma unroll
+    for (int s = 0; s < kSdWords; ++s)
+        v[s] = tid + 256 * s < CW ? ldg<float4>(x + 4 * (tid + 256 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
+    u64 words[kSdWords];
+    bool bad = false;
+    u64 hs = 0;
+#pragma unroll
+    for (int s = 0; s < kSdWords; ++s) {
+        const int w = tid + 256 * s;
+        words[s] = 0;
+        if (w < CW) {
+            words[s] = (u64)sigdig_code(v[s].x, d.qdigits, T, bad) |
+                       ((u64)sigdig_code(v[s].y, d.qdigits, T, bad) << 16) |
+                       ((u64)sigdig_code(v[s].z, d.qdigits, T, bad) << 32) |
+                       ((u64)sigdig_code(v[s].w, d.qdigits, T, bad) << 48);
+            hs += mix64(words[s] ^ ((u64)(w + 1) * kPhi));
+        }
+    }
+    const u64 ws = wave_sum_u64(hs);
+    const bool wbad = __ballot(bad) != 0ull;
+    if (lane == 0) {
+        s_sum[wv] = ws;
+        s_flag[wv] = wbad ? 1 : 0;
+    }
+    __syncthreads();
+    const u64 S = s_sum[0] + s_sum[1] + s_sum[2] + s_sum[3];
+    const bool anybad = (s_flag[0] | s_flag[1] | s_flag[2] | s_flag[3]) != 0;
+    __syncthreads();   // s_flag is reused by the probe
+
+    unsigned err = hbad ? RNNLM_DERR_HANDLE : (anybad ? RNNLM_DERR_VALUE : 0u);
+#pragma unroll
+    for (int c = 0; c < 3; ++c)
+        if (w3[c] < 0 || w3[c] >= d.V) { err |= RNNLM_DERR_WORD; w3[c] = 0; }
+    const int w1 = w3[0];
+    const u64 h = mix64(d.seed ^ S ^ mix64((u64)w1 + 1));
+
+    // history-cache probe; every branch below is uniform over the block
+    int hit = -1;
+    unsigned pos = (unsigned)(h & d.hi_mask);
+    for (unsigned n = 0; n <= d.hi_mask; ++n) {
+        const HcIdx r = d.hc_idx[pos];
+        if (r.slot < 0) break;
+        if (r.hash == h && r.word == w1) {
+            const u64 *cc = d.hc_codes + (size_t)r.slot * CW;
+            bool neq = false;
+#pragma unroll
+            for (int s = 0; s < kSdWords; ++s) {
+                const int w = tid + 256 * s;
+                if (w < CW) neq |= cc[w] != words[s];
+            }
+            const bool wneq = __ballot(neq) != 0ull;
+            if (lane == 0) s_flag[wv] = wneq ? 1 : 0;
+            __syncthreads();
+            const bool eq = (s_flag[0] | s_flag[1] | s_flag[2] | s_flag[3]) == 0;
+            __syncthreads();
+            if (eq) { hit = r.slot; break; }
+        }
+        pos = (pos + 1) & d.hi_mask;
+    }
+
+    u64 *out = d.f_codes + (size_t)i * CW;
+#pragma unroll
+    for (int s = 0; s < kSdWords; ++s) {
+        const int w = tid + 256 * s;
+        if (w < CW) out[w] = words[s];
+    }
+    if (tid == 0) {
+        if (err) atomicOr(d.derr, err);
+        HistRec hr;
+        hr.hash = h;
+        hr.slot = hit;
+        hr.w1 = w1;
+        d.f_hrec[i] = hr;
+        if (f.h_hash) f.h_hash[i] = h;
+    }
+}
+
 // The frames of a launch (one per session) side by side: each role's blocks
 // are split among the frames by the ranges in fb. MULTI = false (a single
 // frame) reads everything at fixed argument offsets, so no argument load
@@ -270,7 +367,10 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d0, FrameBlock fb, DecadeT
     }
     const Dev d = MULTI ? session_view(d0, fb.sess[e]) : d0;
     const FrameArgs &f = fb.f[e];
-    if (role == 0) hist_wave(d, f, T, lb * 4 + wave_id());
+    if (role == 0) {
+        if (d.qmode == RNNLM_Q_SIGDIG) hist_block_sigdig(d, f, T, lb);   // one block per history
+        else hist_wave(d, f, T, lb * 4 + wave_id());                    // one wave per history
+    }
     else if (role == 1) query_key(d, f, lb * blockDim.x + threadIdx.x);
     else if (role == 2) insert_staged(d, lb, fb.soff[e + 1] - fb.soff[e]);
     else fold_counts(d, fb.npart[e]);
