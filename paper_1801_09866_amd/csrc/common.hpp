@@ -94,6 +94,8 @@ struct Dev {
     const void *emb;
     const void *Wp[2];
     const float *b_ih[2];
+    const void *Wl;    // the layer a GRU launch computes: Wp[layer], b_ih[layer] (set per launch, so
+    const float *bl;   // that no argument load waits for the layer index)
     const void *U_out;
     const float *b_out;
     const float *maxent;

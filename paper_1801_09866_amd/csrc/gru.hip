@@ -133,7 +133,7 @@ __device__ __forceinline__ void gru_epilogue(const Dev &d, const Rows &R, int la
                                              const f4_t &anx, const f4_t &anh) {
     const int lane = threadIdx.x & 63;
     const int j = j0 + ub * 16 + (lane & 15);
-    const float *b = d.b_ih[layer];
+    const float *b = d.bl;
     const float br = b[j], bz = b[d.H + j], bn = b[2 * d.H + j];
     // every load first (the stores could alias them as far as the compiler
     // knows, which would serialise one round trip per row)
@@ -217,7 +217,7 @@ __device__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float 
     const int nsteps = K / KS;
     const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;   // scalars
     const int row = lane & 15, kq = (KS / 4) * (lane >> 4);
-    const E *Wp = reinterpret_cast<const E *>(d.Wp[layer]);
+    const E *Wp = reinterpret_cast<const E *>(d.Wl);
     for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
         int mt, jt;
         if ((NJ & 7) == 0) {   // every XCD keeps its own unit tiles (and weights)
@@ -342,7 +342,7 @@ __device__ __forceinline__ void narrow_preload(const Dev &d, const SessList &sl,
     const int tid = threadIdx.x, col = tid & 15;
     // a fixed set of loads, none behind a branch
     const int j = 4 * g + (tid & 3);
-    const float *bb = d.b_ih[layer];
+    const float *bb = d.bl;
     p.br = ldg<float>(bb + j);
     p.bz = ldg<float>(bb + d.H + j);
     p.bn = ldg<float>(bb + 2 * d.H + j);
@@ -376,7 +376,7 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
     // the epilogue never reads them (an MFMA output column depends only on
     // its own B column)
     const int gate = col >> 2, j0 = 4 * g;
-    const E *wrow = reinterpret_cast<const E *>(d.Wp[layer]) + (size_t)((gate < 3 ? gate : 0) * d.H + j0 + (col & 3)) * K + kq;
+    const E *wrow = reinterpret_cast<const E *>(d.Wl) + (size_t)((gate < 3 ? gate : 0) * d.H + j0 + (col & 3)) * K + kq;
     const int nt = (M + 15) >> 4;         // row tiles (block-uniform)
     const bool pre_rows = USE_PRE && R.n == 1;   // block-uniform
 
@@ -392,7 +392,7 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
             ebz = pre.bz;
             ebn = pre.bn;
         } else {
-            const float *bb = d.b_ih[layer];
+            const float *bb = d.bl;
             ebr = bb[j];
             ebz = bb[d.H + j];
             ebn = bb[2 * d.H + j];
@@ -522,7 +522,7 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
-    const float *Wp = reinterpret_cast<const float *>(d.Wp[layer]);
+    const float *Wp = reinterpret_cast<const float *>(d.Wl);
 
     // A loader: row tid/8, 4 consecutive k at (tid%8)*4 and 32 further on.
     // Rows past M load row M - 1 (m0 < M): their products only reach output
@@ -636,7 +636,7 @@ __device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, flo
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
-    const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wp[layer]);
+    const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
 
     const int a_row = tid >> 3, a_k = (tid & 7) * 8;
     const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
@@ -714,8 +714,8 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
     __shared__ __align__(16) float smem[G_LDS_FLOATS];
     // the narrow path's unit group of a block index: each XCD its own contiguous share
     const int NB = d.H / 4;
-    const bool by_xcd = ((NB & 7) == 0) & ((int)gridDim.x >= NB);   // no branch: a select
-    auto group = [&](int t) { return by_xcd ? (t & 7) * (NB >> 3) + (t >> 3) : t; };
+    const int by_xcd = ((NB & 7) == 0) & ((int)gridDim.x >= NB);   // arithmetic, not a branch
+    auto group = [&](int t) { return t + by_xcd * ((t & 7) * (NB >> 3) + (t >> 3) - t); };
     NarrowPre<BF16W> pre;
     Rows R;
     if (ONE) {
@@ -792,8 +792,11 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
                                        d.wdtype == RNNLM_BF16 ? 2 : 4);
 }
 
-void launch_gru_layer(const Dev &d, const FrameBlock &fb, int layer, int max_rows, hipStream_t s, Stamp ts) {
+void launch_gru_layer(const Dev &d0, const FrameBlock &fb, int layer, int max_rows, hipStream_t s, Stamp ts) {
     if (max_rows <= 0) return;
+    Dev d = d0;
+    d.Wl = d0.Wp[layer];
+    d.bl = d0.b_ih[layer];
     SessList sl;
     sl.n = fb.n;
     for (int e = 0; e < kMaxSessions; ++e) sl.sess[e] = e < fb.n ? fb.sess[e] : 0;
