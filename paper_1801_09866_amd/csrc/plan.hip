@@ -188,27 +188,30 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
     const int RQ = (nq + PT - 1) / PT;    // active query rounds (block-uniform)
 
     // ---------------- one round of independent loads ----------------
-    long long ctr_v = 0;
-    if (tid < C_N) ctr_v = d.ctr[tid];
+    // clamped, unconditional loads: no branch between the argument loads and
+    // these, and idle elements all read one in-bounds element
+    const long long ctr_v = ldg<long long>(d.ctr + min(tid, C_N - 1));
     const int hlast = n > 0 ? n - 1 : 0;
     u64 h_hash[HR], h_hp[HR];
     int h_slot[HR], h_w1[HR];
 #pragma unroll
     for (int r = 0; r < HR; ++r) {
-        const int i = min(tid + r * PT, hlast);   // clamped: no divergent loads
+        const int i = min(tid + r * PT, hlast);
         const HistRec hr = d.f_hrec[i];   // one 16-byte load per history
         h_hash[r] = hr.hash;
         h_slot[r] = hr.slot;
         h_w1[r] = hr.w1;
-        h_hp[r] = f.hist_ptr ? f.hist_ptr[i] : 0;   // handles are checked where they are used
     }
     int4 qk[QR];
     const int qlast = nq > 0 ? nq - 1 : 0;
 #pragma unroll
-    for (int r = 0; r < QR; ++r) {   // clamped, unconditional: idle rounds all read one element
+    for (int r = 0; r < QR; ++r) {
         const int q = min(tid + r * PT, qlast);
         qk[r] = d.f_qkey[q];
     }
+#pragma unroll
+    for (int r = 0; r < HR; ++r)   // handles are checked where they are used
+        h_hp[r] = f.hist_ptr ? f.hist_ptr[min(tid + r * PT, hlast)] : 0;
 
     // ---------------- race tables (block-uniform sizes) ----------------
     // first tables at load <= 1/4, else the query one, then the history one,
