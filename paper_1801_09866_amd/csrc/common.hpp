@@ -76,6 +76,11 @@ struct HistRec {
     int w1;     // GRU input word (clamped into [0, V))
 };
 
+// Cache probes read the linear-probe sequence kProbeWin records at a time,
+// one record per lane (tables have at least 64 slots).
+constexpr int kProbeShift = 4;
+constexpr int kProbeWin = 1 << kProbeShift;
+
 // Independent decode sessions per context (one frame each per launch).
 constexpr int kMaxSessions = 8;
 

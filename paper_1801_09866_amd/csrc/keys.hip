@@ -196,14 +196,21 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     const int w1 = w3[0];
     const u64 h = mix64(d.seed ^ S ^ mix64((u64)w1 + 1));
 
-    // history-cache probe: one 16-byte record per step, then an exact check
+    // history-cache probe: the linear-probe sequence from the key's position,
+    // kProbeWin index records per round trip (one per lane); a record with the
+    // key's hash and word before the first empty one is confirmed by an exact
+    // comparison of the codes
     int hit = -1;
-    unsigned pos = (unsigned)(h & d.hi_mask);
-    for (unsigned n = 0; n <= d.hi_mask; ++n) {
-        const HcIdx r = d.hc_idx[pos];
-        if (r.slot < 0) break;
-        if (r.hash == h && r.word == w1) {
-            const u64 *cc = d.hc_codes + (size_t)r.slot * CW;
+    unsigned base = (unsigned)(h & d.hi_mask);
+    for (unsigned n = 0; n <= (d.hi_mask >> kProbeShift) && hit < 0; ++n) {
+        const HcIdx r = d.hc_idx[(base + (lane & (kProbeWin - 1))) & d.hi_mask];
+        const bool in = lane < kProbeWin;
+        const u64 emp = __ballot(in && r.slot < 0);
+        u64 cand = __ballot(in && r.slot >= 0 && r.hash == h && r.word == w1);
+        if (emp) cand &= (emp & (~emp + 1ull)) - 1ull;
+        for (; cand; cand &= cand - 1ull) {
+            const int slot = __shfl(r.slot, __ffsll((unsigned long long)cand) - 1);
+            const u64 *cc = d.hc_codes + (size_t)slot * CW;
             bool neq = false;
             if (d.qmode == RNNLM_Q_SIGN) {
                 if (lane < CW) neq = cc[lane] != words[0];
@@ -214,9 +221,10 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
                     if (w < CW) neq |= cc[w] != words[s];
                 }
             }
-            if (__ballot(neq) == 0ull) { hit = r.slot; break; }
+            if (__ballot(neq) == 0ull) { hit = slot; break; }
         }
-        pos = (pos + 1) & d.hi_mask;
+        if (emp) break;
+        base = (base + kProbeWin) & d.hi_mask;
     }
 
     // per-frame outputs
@@ -297,14 +305,19 @@ __device__ void hist_block_sigdig(const Dev &d, const FrameArgs &f, const Decade
     const int w1 = w3[0];
     const u64 h = mix64(d.seed ^ S ^ mix64((u64)w1 + 1));
 
-    // history-cache probe; every branch below is uniform over the block
+    // history-cache probe in windows, as in hist_wave; every wave reads the
+    // same records, so every branch below is uniform over the block
     int hit = -1;
-    unsigned pos = (unsigned)(h & d.hi_mask);
-    for (unsigned n = 0; n <= d.hi_mask; ++n) {
-        const HcIdx r = d.hc_idx[pos];
-        if (r.slot < 0) break;
-        if (r.hash == h && r.word == w1) {
-            const u64 *cc = d.hc_codes + (size_t)r.slot * CW;
+    unsigned base = (unsigned)(h & d.hi_mask);
+    for (unsigned n = 0; n <= (d.hi_mask >> kProbeShift) && hit < 0; ++n) {
+        const HcIdx r = d.hc_idx[(base + (lane & (kProbeWin - 1))) & d.hi_mask];
+        const bool in = lane < kProbeWin;
+        const u64 emp = __ballot(in && r.slot < 0);
+        u64 cand = __ballot(in && r.slot >= 0 && r.hash == h && r.word == w1);
+        if (emp) cand &= (emp & (~emp + 1ull)) - 1ull;
+        for (; cand; cand &= cand - 1ull) {
+            const int slot = __shfl(r.slot, __ffsll((unsigned long long)cand) - 1);
+            const u64 *cc = d.hc_codes + (size_t)slot * CW;
             bool neq = false;
 #pragma unroll
             for (int s = 0; s < kSdWords; ++s) {
@@ -316,9 +329,10 @@ __device__ void hist_block_sigdig(const Dev &d, const FrameArgs &f, const Decade
             __syncthreads();
             const bool eq = (s_flag[0] | s_flag[1] | s_flag[2] | s_flag[3]) == 0;
             __syncthreads();
-            if (eq) { hit = r.slot; break; }
+            if (eq) { hit = slot; break; }
         }
-        pos = (pos + 1) & d.hi_mask;
+        if (emp) break;
+        base = (base + kProbeWin) & d.hi_mask;
     }
 
     u64 *out = d.f_codes + (size_t)i * CW;

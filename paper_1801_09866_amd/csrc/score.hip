@@ -46,8 +46,10 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
     // once: the LM cache's first probe record (for a cached history key), the
     // output row, the history row, the bias and the MaxEnt weights. A hit
     // wastes the row loads but saves the round trip a miss would wait for.
-    unsigned pos = (unsigned)(query_hash((u64)rec.hs, key.y, key.z, t) & d.si_mask);
-    ScEnt e = d.sc_tab[probe ? pos : 0];
+    // the LM cache's linear-probe sequence from the key's position, kProbeWin
+    // records at a time (lane l reads record l of the window)
+    unsigned base = (unsigned)(query_hash((u64)rec.hs, key.y, key.z, t) & d.si_mask);
+    ScEnt e = d.sc_tab[probe ? (base + (lane & (kProbeWin - 1))) & d.si_mask : 0];
     const float *h = reinterpret_cast<const float *>(rec.hptr);
     float acc = 0.0f;
     if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
@@ -100,12 +102,21 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
     for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)];
     bool hit = false;
     float s = 0.0f;
-    if (probe) {
-        for (unsigned k = 0; k <= d.si_mask; ++k) {
-            if (e.hs < 0) break;
-            if (e.hs == rec.hs && e.w2 == key.y && e.w3 == key.z && e.t == t) { hit = true; s = e.val; break; }
-            pos = (pos + 1) & d.si_mask;
-            e = d.sc_tab[pos];
+    if (probe) {   // the first matching record before the first empty one
+        for (unsigned k = 0; k <= (d.si_mask >> kProbeShift); ++k) {
+            const bool in = lane < kProbeWin;
+            const u64 stop = __ballot(in && (e.hs < 0 || (e.hs == rec.hs && e.w2 == key.y && e.w3 == key.z &&
+                                                             e.t == t)));
+            if (stop) {
+                const int f = __ffsll((unsigned long long)stop) - 1;
+                const int hs_f = __shfl(e.hs, f);
+                const float v_f = __shfl(e.val, f);
+                hit = hs_f >= 0;
+                s = v_f;
+                break;
+            }
+            base = (base + kProbeWin) & d.si_mask;
+            e = d.sc_tab[(base + (lane & (kProbeWin - 1))) & d.si_mask];
         }
     }
     if (!hit) s = wave_sum(acc) + me;
