@@ -1,6 +1,7 @@
 """GPU edge cases against the oracle: empty and ragged frames, frames at the
 configured maxima, duplicates, tiny cache capacities, repeated frames, the
-saturated-update-gate invariant, and the sticky device error path."""
+saturated-update-gate invariant, the sticky device error path, and MaxEnt
+slots revealed exactly by an index-valued table."""
 import numpy as np
 import pytest
 import torch
@@ -195,3 +196,29 @@ def test_gru_paths_by_row_count(L, wd):
         assert ok, "rows %d: GRU outputs differ by %.3g" % (n_h, err)
         ok, err = close(out["scores"][:len(qh)].cpu().numpy(), res.scores, *tol)
         assert ok, "rows %d: scores differ by %.3g" % (n_h, err)
+
+
+@pytest.mark.parametrize("order", [2, 3, 4])
+def test_maxent_slots_revealed_by_an_index_table(order):
+    """Zero output layer and lambda[i] = i (exact in fp32 for 2^16 slots),
+    one n-gram order at a time: each computed score is the slot the device's
+    MaxEnt hash picks, which must equal the oracle's index of the n-gram
+    (orders 2..order all add; subtracting the lower orders isolates the top
+    one)."""
+    from oracle.rnnlm_oracle import maxent_index
+    m = ModelCfg(V=5000, E=64, H=128, L=1, wdtype=F32, maxent_log2=16, maxent_order=order)
+    rng = np.random.default_rng(70 + order)
+    w = weights(m, rng)
+    w["U_out"][:] = 0
+    w["b_out"][:] = 0
+    w["maxent"] = np.arange(1 << 16, dtype=np.float32)
+    b = Both(m, w, Q_SIGN)
+    vec, words, qh, qt = rand_frame(rng, m, 40, 300)
+    out, res = b.frame(vec, words, qh, qt, "index table, order %d" % order)
+    comp = res.q_status == 0   # computed queries carry their own sum
+    want = np.zeros(len(qt))
+    for o in range(2, order + 1):
+        ctx = [words[qh, c] for c in range(o - 1)]
+        want += maxent_index(o, ctx, qt, 16).astype(np.float64)
+    got = out["scores"][:len(qt)].cpu().numpy().astype(np.float64)
+    assert np.array_equal(got[comp], want[comp])
