@@ -618,11 +618,16 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
 }
 
 // ------------------------------- bf16 -------------------------------------
-constexpr int H_BK = 64;
-constexpr int H_LDA = H_BK + 8;   // padded LDS row (bf16 elements)
-
-
+// A bf16 K step is little MFMA work (a 64-wide step is 6 MFMAs of 16 cycles
+// per wave), so the tile is bound by how many bytes are in flight, not by the
+// matrix units: the step is 128 wide where E and H allow it, and two register
+// stages keep two steps' loads in flight. fp32 operand rows stay fp32 in the
+// stage and are rounded to bf16 when they are written to LDS, so that no
+// arithmetic waits on a load before its step.
+template <int BK>
 __device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
+    constexpr int LDA = BK + 8;          // padded LDS row (bf16 elements)
+    constexpr int AC = BK / 64;          // A chunks of 8 elements per thread (rows tid/8)
     const int NJ = d.H / G_BJ;
     int mt, jt;
     gru_tile_of(tile, NJ, mt, jt);
@@ -630,71 +635,101 @@ __device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, flo
     if (m0 >= M) return;
 
     uint16_t *sm16 = reinterpret_cast<uint16_t *>(smem);
-    auto As = reinterpret_cast<uint16_t (*)[G_BM][H_LDA]>(sm16);
-    auto Bs = reinterpret_cast<uint16_t (*)[3 * G_BJ][H_LDA]>(sm16 + 2 * G_BM * H_LDA);
+    auto As = reinterpret_cast<uint16_t (*)[G_BM][LDA]>(sm16);
+    auto Bs = reinterpret_cast<uint16_t (*)[3 * G_BJ][LDA]>(sm16 + 2 * G_BM * LDA);
 
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
 
+    // A: row tid/8, chunks of 8 elements at (tid%8)*8 + 64c. Rows past M read
+    // row M - 1: their products only reach rows the epilogue does not write.
     const int a_row = tid >> 3, a_k = (tid & 7) * 8;
-    const RowSrc src = row_source(d, R, layer, m0 + a_row, M);
-    const int b_k = (tid & 7) * 8;
-    const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
-    const uint16_t *bp0 = Wp + (size_t)((b_r0 / G_BJ) * d.H + j0 + (b_r0 % G_BJ)) * K + b_k;
-    const uint16_t *bp1 = Wp + (size_t)((b_r1 / G_BJ) * d.H + j0 + (b_r1 % G_BJ)) * K + b_k;
-    const bool has_b1 = b_r1 < 3 * G_BJ;
+    const RowSrc src = row_source(d, R, layer, min(m0 + a_row, M - 1), M);
+    // B: 96 rows x BK/8 chunks over 512 threads. Rows tid/8 take chunks
+    // (tid%8) + 8c for c < BK/64; with BK = 128 the last 32 rows take one
+    // chunk per thread as well.
+    const int b_r0 = tid >> 3, b_k0 = (tid & 7) * 8;
+    const int b_r1 = BK == 128 ? 64 + (tid >> 4) : 64 + (tid >> 3), b_k1 = BK == 128 ? (tid & 15) * 8 : (tid & 7) * 8;
+    const bool has_b1 = BK == 128 ? true : b_r1 < 3 * G_BJ;
+    auto wrow = [&](int r) { return Wp + (size_t)((r / G_BJ) * d.H + j0 + (r % G_BJ)) * K; };
+    const uint16_t *bp0 = wrow(b_r0) + b_k0, *bp1 = wrow(has_b1 ? b_r1 : 0) + b_k1;
 
-    uint4 ra, rb0, rb1;
-    auto load = [&](int k0) {
-        const int k = k0 + a_k;
-        if (!src.valid) {
-            ra = make_uint4(0, 0, 0, 0);
-        } else if (k < Kx) {
-            if (src.x_bf16) {
-                ra = ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k);
-            } else {
-                const float *p = reinterpret_cast<const float *>(src.x) + k;
-                ra = pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4));
-            }
-        } else {
-            const float *p = src.h + (k - Kx);
-            ra = pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4));
-        }
-        rb0 = ldg<uint4>(bp0 + k0);
-        if (has_b1) rb1 = ldg<uint4>(bp1 + k0);
+    struct Stage {
+        float4 a[2 * AC];   // fp32 source: two float4 per chunk; bf16 source: one uint4 per chunk in a[c]
+        uint4 b0[AC], b1;
     };
-    auto store = [&](int buf) {
-        *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k]) = ra;
-        *reinterpret_cast<uint4 *>(&Bs[buf][b_r0][b_k]) = rb0;
-        if (has_b1) *reinterpret_cast<uint4 *>(&Bs[buf][b_r1][b_k]) = rb1;
+    auto load = [&](Stage &S, int k0) {   // a K step lies wholly in the input part or the history part
+        const bool xp = k0 < Kx;          // uniform
+        if (xp && src.x_bf16) {
+            const uint16_t *p = reinterpret_cast<const uint16_t *>(src.x) + k0 + a_k;
+#pragma unroll
+            for (int c = 0; c < AC; ++c) S.a[c] = __builtin_bit_cast(float4, ldg<uint4>(p + 64 * c));
+        } else {
+            const float *p = (xp ? reinterpret_cast<const float *>(src.x) + k0 : src.h + (k0 - Kx)) + a_k;
+#pragma unroll
+            for (int c = 0; c < AC; ++c) {
+                S.a[2 * c] = ldg<float4>(p + 64 * c);
+                S.a[2 * c + 1] = ldg<float4>(p + 64 * c + 4);
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < AC; ++c) S.b0[c] = ldg<uint4>(bp0 + k0 + 64 * c);
+        if (has_b1) S.b1 = ldg<uint4>(bp1 + k0);
+    };
+    auto store = [&](const Stage &S, int buf, int k0) {
+        const bool raw16 = k0 < Kx && src.x_bf16;   // uniform
+#pragma unroll
+        for (int c = 0; c < AC; ++c) {
+            const uint4 v = raw16 ? __builtin_bit_cast(uint4, S.a[c]) : pack_bf16x8(S.a[2 * c], S.a[2 * c + 1]);
+            *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k + 64 * c]) = v;
+            *reinterpret_cast<uint4 *>(&Bs[buf][b_r0][b_k0 + 64 * c]) = S.b0[c];
+        }
+        if (has_b1) *reinterpret_cast<uint4 *>(&Bs[buf][b_r1][b_k1]) = S.b1;
     };
 
     f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
     const int rb = w & 3, ub = w >> 2;
     const int fr = lane & 15, fk = 8 * (lane >> 4);
-
-    const int nk = K / H_BK;
-    load(0);
-    store(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load((kt + 1) * H_BK);
-        const bool xphase = kt * H_BK < Kx;
+    auto compute = [&](int buf, bool xphase) {
+        bf8_t a[BK / 32], br[BK / 32], bz[BK / 32], bn[BK / 32];
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-            const bf8_t a = *reinterpret_cast<const bf8_t *>(&As[buf][rb * 16 + fr][hh * 32 + fk]);
-            const bf8_t br = *reinterpret_cast<const bf8_t *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-            const bf8_t bz = *reinterpret_cast<const bf8_t *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-            const bf8_t bn = *reinterpret_cast<const bf8_t *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-            ar = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, br, ar, 0, 0, 0);
-            az = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bz, az, 0, 0, 0);
-            if (xphase) anx = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bn, anx, 0, 0, 0);
-            else anh = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bn, anh, 0, 0, 0);
+        for (int hh = 0; hh < BK / 32; ++hh) {
+            a[hh] = *reinterpret_cast<const bf8_t *>(&As[buf][rb * 16 + fr][hh * 32 + fk]);
+            br[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
+            bz[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
+            bn[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
         }
-        if (kt + 1 < nk) store(buf ^ 1);
+        f4_t an = xphase ? anx : anh;
+#pragma unroll
+        for (int hh = 0; hh < BK / 32; ++hh) {
+            ar = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], br[hh], ar, 0, 0, 0);
+            az = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], bz[hh], az, 0, 0, 0);
+            an = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], bn[hh], an, 0, 0, 0);
+        }
+        if (xphase) anx = an;
+        else anh = an;
+    };
+
+    // S0 carries the odd steps and S1 the even ones from step 2 on; LDS buffer
+    // s & 1 holds step s
+    const int nk = K / BK;   // >= 2
+    Stage S0, S1;
+    load(S0, 0);
+    store(S0, 0, 0);
+    load(S0, BK);
+    if (nk > 2) load(S1, 2 * BK);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+        compute(0, kt * BK < Kx);
+        if (kt + 1 < nk) store(S0, 1, (kt + 1) * BK);
+        if (kt + 3 < nk) load(S0, (kt + 3) * BK);
+        __syncthreads();
+        if (kt + 1 >= nk) break;
+        compute(1, (kt + 1) * BK < Kx);
+        if (kt + 2 < nk) store(S1, 0, (kt + 2) * BK);
+        if (kt + 4 < nk) load(S1, (kt + 4) * BK);
         __syncthreads();
     }
     gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
@@ -704,7 +739,7 @@ __device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, flo
 static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
 static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles exceed the LDS buffer");
 static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
-static_assert((2 * G_BM * H_LDA + 2 * 3 * G_BJ * H_LDA) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
+static_assert((2 * G_BM * (128 + 8) + 2 * 3 * G_BJ * (128 + 8)) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
 // ONE: the launch scores a single frame (the host knows), so the row lists
 // need no per-frame selection and the narrow path's operands can be loaded
@@ -758,7 +793,10 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
     } else {                          // 64 x 32 MFMA tiles through LDS
         const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / G_BJ);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (BF16W) gru_mfma_bf16(d, R, layer, M, smem, t);
+            if (BF16W) {   // a 128-wide K step when both parts of K split into them (uniform)
+                if ((((layer == 0 ? d.E : d.H) | d.H) & 127) == 0) gru_mfma_bf16<128>(d, R, layer, M, smem, t);
+                else gru_mfma_bf16<64>(d, R, layer, M, smem, t);
+            }
             else gru_mfma_f32(d, R, layer, M, smem, t);
         }
     }

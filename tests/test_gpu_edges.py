@@ -175,11 +175,13 @@ def test_host_rejects_oversized_frames():
     assert e.value.code == R.EINVAL
 
 
-@pytest.mark.parametrize("L,wd", [(1, F32), (2, F32), (1, 1)])
-def test_gru_paths_by_row_count(L, wd):
+@pytest.mark.parametrize("L,wd,E,H", [(1, F32, 128, 256), (2, F32, 128, 256), (1, 1, 128, 256), (2, 1, 192, 320)])
+def test_gru_paths_by_row_count(L, wd, E, H):
     """Row counts on each side of the narrow (<= 32), medium (<= 256) and
-    64 x 32 tile paths, all new keys, against the oracle."""
-    m = ModelCfg(V=3000, E=128, H=256, L=L, wdtype=wd, maxent_log2=12, maxent_order=4)
+    64 x 32 tile paths, all new keys, against the oracle. The bf16 tile path
+    steps 128 wide through K when E and H are multiples of 128 and 64 wide
+    otherwise (the last case)."""
+    m = ModelCfg(V=3000, E=E, H=H, L=L, wdtype=wd, maxent_log2=12, maxent_order=4)
     rng = np.random.default_rng(10 + L + 3 * wd)
     w = weights(m, rng, scale=0.08)
     tol = (2e-2, 0.0) if wd == 1 else (ATOL, RTOL)
