@@ -618,128 +618,125 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
 }
 
 // ------------------------------- bf16 -------------------------------------
-// A bf16 K step is little MFMA work (a 64-wide step is 6 MFMAs of 16 cycles
-// per wave), so the tile is bound by how many bytes are in flight, not by the
-// matrix units: the step is 128 wide where E and H allow it, and two register
-// stages keep two steps' loads in flight. fp32 operand rows stay fp32 in the
-// stage and are rounded to bf16 when they are written to LDS, so that no
-// arithmetic waits on a load before its step.
-template <int BK>
-__device__ void gru_mfma_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
-    constexpr int LDA = BK + 8;          // padded LDS row (bf16 elements)
-    constexpr int AC = BK / 64;          // A chunks of 8 elements per thread (rows tid/8)
-    const int NJ = d.H / G_BJ;
+// A bf16 K step is little MFMA work for the bytes it loads, so this tile is
+// bound by the bytes it has in flight rather than by the matrix units. fp32
+// operand rows stay fp32 in the register stage and are rounded to bf16 when
+// written to LDS, so that no arithmetic waits on a load before its step.
+// bf16 tile of 64 rows x 64 hidden units (three gates: 192 weight rows),
+// 64-wide K steps, two register stages. Against the 64 x 32 tile it reads
+// each operand row half as often and moves fewer bytes per MFMA; each wave
+// owns 16 rows and two 16-unit blocks.
+constexpr int W_BJ = 64, W_BK = 64, W_LDA = W_BK + 8;
+static_assert((2 * G_BM * W_LDA + 2 * 3 * W_BJ * W_LDA) / 2 <= G_LDS_FLOATS, "wide bf16 tiles exceed the LDS buffer");
+
+__device__ void gru_mfma_bf16w(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
+    const int NJ = d.H / W_BJ;
     int mt, jt;
     gru_tile_of(tile, NJ, mt, jt);
-    const int m0 = mt * G_BM, j0 = jt * G_BJ;
+    const int m0 = mt * G_BM, j0 = jt * W_BJ;
     if (m0 >= M) return;
 
     uint16_t *sm16 = reinterpret_cast<uint16_t *>(smem);
-    auto As = reinterpret_cast<uint16_t (*)[G_BM][LDA]>(sm16);
-    auto Bs = reinterpret_cast<uint16_t (*)[3 * G_BJ][LDA]>(sm16 + 2 * G_BM * LDA);
+    auto As = reinterpret_cast<uint16_t (*)[G_BM][W_LDA]>(sm16);
+    auto Bs = reinterpret_cast<uint16_t (*)[3 * W_BJ][W_LDA]>(sm16 + 2 * G_BM * W_LDA);
 
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
 
-    // A: row tid/8, chunks of 8 elements at (tid%8)*8 + 64c. Rows past M read
-    // row M - 1: their products only reach rows the epilogue does not write.
+    // A: row tid/8, 8 elements at (tid%8)*8; rows past M read row M - 1
     const int a_row = tid >> 3, a_k = (tid & 7) * 8;
     const RowSrc src = row_source(d, R, layer, min(m0 + a_row, M - 1), M);
-    // B: 96 rows x BK/8 chunks over 512 threads. Rows tid/8 take chunks
-    // (tid%8) + 8c for c < BK/64; with BK = 128 the last 32 rows take one
-    // chunk per thread as well.
-    const int b_r0 = tid >> 3, b_k0 = (tid & 7) * 8;
-    const int b_r1 = BK == 128 ? 64 + (tid >> 4) : 64 + (tid >> 3), b_k1 = BK == 128 ? (tid & 15) * 8 : (tid & 7) * 8;
-    const bool has_b1 = BK == 128 ? true : b_r1 < 3 * G_BJ;
-    auto wrow = [&](int r) { return Wp + (size_t)((r / G_BJ) * d.H + j0 + (r % G_BJ)) * K; };
-    const uint16_t *bp0 = wrow(b_r0) + b_k0, *bp1 = wrow(has_b1 ? b_r1 : 0) + b_k1;
+    // B: weight rows tid/8 + 64c (c < 3: one per gate), same 8 elements
+    const uint16_t *bp[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) bp[c] = Wp + (size_t)(c * d.H + j0 + (tid >> 3)) * K + a_k;
 
     struct Stage {
-        float4 a[2 * AC];   // fp32 source: two float4 per chunk; bf16 source: one uint4 per chunk in a[c]
-        uint4 b0[AC], b1;
+        float4 a[2];   // fp32 source; a bf16 source keeps its 8 elements in a[0]
+        uint4 b[3];
     };
     auto load = [&](Stage &S, int k0) {   // a K step lies wholly in the input part or the history part
-        const bool xp = k0 < Kx;          // uniform
-        if (xp && src.x_bf16) {
-            const uint16_t *p = reinterpret_cast<const uint16_t *>(src.x) + k0 + a_k;
-#pragma unroll
-            for (int c = 0; c < AC; ++c) S.a[c] = __builtin_bit_cast(float4, ldg<uint4>(p + 64 * c));
+        if (k0 < Kx && src.x_bf16) {      // uniform
+            S.a[0] = __builtin_bit_cast(float4, ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k0 + a_k));
         } else {
-            const float *p = (xp ? reinterpret_cast<const float *>(src.x) + k0 : src.h + (k0 - Kx)) + a_k;
-#pragma unroll
-            for (int c = 0; c < AC; ++c) {
-                S.a[2 * c] = ldg<float4>(p + 64 * c);
-                S.a[2 * c + 1] = ldg<float4>(p + 64 * c + 4);
-            }
+            const float *p = (k0 < Kx ? reinterpret_cast<const float *>(src.x) + k0 : src.h + (k0 - Kx)) + a_k;
+            S.a[0] = ldg<float4>(p);
+            S.a[1] = ldg<float4>(p + 4);
         }
 #pragma unroll
-        for (int c = 0; c < AC; ++c) S.b0[c] = ldg<uint4>(bp0 + k0 + 64 * c);
-        if (has_b1) S.b1 = ldg<uint4>(bp1 + k0);
+        for (int c = 0; c < 3; ++c) S.b[c] = ldg<uint4>(bp[c] + k0);
     };
     auto store = [&](const Stage &S, int buf, int k0) {
         const bool raw16 = k0 < Kx && src.x_bf16;   // uniform
+        *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k]) =
+            raw16 ? __builtin_bit_cast(uint4, S.a[0]) : pack_bf16x8(S.a[0], S.a[1]);
 #pragma unroll
-        for (int c = 0; c < AC; ++c) {
-            const uint4 v = raw16 ? __builtin_bit_cast(uint4, S.a[c]) : pack_bf16x8(S.a[2 * c], S.a[2 * c + 1]);
-            *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k + 64 * c]) = v;
-            *reinterpret_cast<uint4 *>(&Bs[buf][b_r0][b_k0 + 64 * c]) = S.b0[c];
-        }
-        if (has_b1) *reinterpret_cast<uint4 *>(&Bs[buf][b_r1][b_k1]) = S.b1;
+        for (int c = 0; c < 3; ++c) *reinterpret_cast<uint4 *>(&Bs[buf][64 * c + (tid >> 3)][a_k]) = S.b[c];
     };
 
-    f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-    const int rb = w & 3, ub = w >> 2;
+    f4_t acc[2][4];   // [unit block][r, z, n input part, n history part]
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[q][g] = f4_t{0, 0, 0, 0};
+    const int rb = w & 3, ub = w >> 2;   // unit blocks ub and ub + 2
     const int fr = lane & 15, fk = 8 * (lane >> 4);
     auto compute = [&](int buf, bool xphase) {
-        bf8_t a[BK / 32], br[BK / 32], bz[BK / 32], bn[BK / 32];
+        bf8_t a[2], b[2][2][3];
 #pragma unroll
-        for (int hh = 0; hh < BK / 32; ++hh) {
+        for (int hh = 0; hh < 2; ++hh) {
             a[hh] = *reinterpret_cast<const bf8_t *>(&As[buf][rb * 16 + fr][hh * 32 + fk]);
-            br[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-            bz[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-            bn[hh] = *reinterpret_cast<const bf8_t *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 32 + fk]);
-        }
-        f4_t an = xphase ? anx : anh;
 #pragma unroll
-        for (int hh = 0; hh < BK / 32; ++hh) {
-            ar = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], br[hh], ar, 0, 0, 0);
-            az = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], bz[hh], az, 0, 0, 0);
-            an = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], bn[hh], an, 0, 0, 0);
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int g = 0; g < 3; ++g)
+                    b[hh][q][g] = *reinterpret_cast<const bf8_t *>(&Bs[buf][g * W_BJ + (ub + 2 * q) * 16 + fr][hh * 32 + fk]);
         }
-        if (xphase) anx = an;
-        else anh = an;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            f4_t an = xphase ? acc[q][2] : acc[q][3];
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh) {
+                acc[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][0], acc[q][0], 0, 0, 0);
+                acc[q][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][1], acc[q][1], 0, 0, 0);
+                an = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][2], an, 0, 0, 0);
+            }
+            if (xphase) acc[q][2] = an;
+            else acc[q][3] = an;
+        }
     };
 
     // S0 carries the odd steps and S1 the even ones from step 2 on; LDS buffer
     // s & 1 holds step s
-    const int nk = K / BK;   // >= 2
+    const int nk = K / W_BK;   // >= 2
     Stage S0, S1;
     load(S0, 0);
     store(S0, 0, 0);
-    load(S0, BK);
-    if (nk > 2) load(S1, 2 * BK);
+    load(S0, W_BK);
+    if (nk > 2) load(S1, 2 * W_BK);
     __syncthreads();
     for (int kt = 0; kt < nk; kt += 2) {
-        compute(0, kt * BK < Kx);
-        if (kt + 1 < nk) store(S0, 1, (kt + 1) * BK);
-        if (kt + 3 < nk) load(S0, (kt + 3) * BK);
+        compute(0, kt * W_BK < Kx);
+        if (kt + 1 < nk) store(S0, 1, (kt + 1) * W_BK);
+        if (kt + 3 < nk) load(S0, (kt + 3) * W_BK);
         __syncthreads();
         if (kt + 1 >= nk) break;
-        compute(1, (kt + 1) * BK < Kx);
-        if (kt + 2 < nk) store(S1, 0, (kt + 2) * BK);
-        if (kt + 4 < nk) load(S1, (kt + 4) * BK);
+        compute(1, (kt + 1) * W_BK < Kx);
+        if (kt + 2 < nk) store(S1, 0, (kt + 2) * W_BK);
+        if (kt + 4 < nk) load(S1, (kt + 4) * W_BK);
         __syncthreads();
     }
-    gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        gru_epilogue(d, R, layer, M, m0, j0, rb, ub + 2 * q, acc[q][0], acc[q][1], acc[q][2], acc[q][3]);
 }
 
 // One launch per layer; the device-side row count picks the path.
 static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
 static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles exceed the LDS buffer");
 static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
-static_assert((2 * G_BM * (128 + 8) + 2 * 3 * G_BJ * (128 + 8)) / 2 <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
 // ONE: the launch scores a single frame (the host knows), so the row lists
 // need no per-frame selection and the narrow path's operands can be loaded
@@ -790,13 +787,10 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
         gru_medium<BF16W>(d, R, layer, M, smem);
-    } else {                          // 64 x 32 MFMA tiles through LDS
-        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / G_BJ);
+    } else {                          // 64 x 32 (fp32) or 64 x 64 (bf16) MFMA tiles through LDS
+        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / (BF16W ? W_BJ : G_BJ));
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (BF16W) {   // a 128-wide K step when both parts of K split into them (uniform)
-                if ((((layer == 0 ? d.E : d.H) | d.H) & 127) == 0) gru_mfma_bf16<128>(d, R, layer, M, smem, t);
-                else gru_mfma_bf16<64>(d, R, layer, M, smem, t);
-            }
+            if (BF16W) gru_mfma_bf16w(d, R, layer, M, smem, t);
             else gru_mfma_f32(d, R, layer, M, smem, t);
         }
     }
