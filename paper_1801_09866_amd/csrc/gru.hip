@@ -21,7 +21,6 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
 
 constexpr int G_BM = 64;    // work-list rows per block
-constexpr int G_BJ = 32;    // hidden units per block (x 3 gates)
 constexpr int G_THREADS = 512;
 
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
@@ -171,7 +170,7 @@ __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
 }
 
 // One LDS buffer serves every path.
-constexpr int G_LDS_FLOATS = 24576;   // 96 KB
+constexpr int G_LDS_FLOATS = 27648;   // 108 KB
 
 // ------------------------ medium path (32 < rows <= 256) -------------------
 // Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
@@ -205,7 +204,7 @@ __device__ __forceinline__ f4_t md_mfma(uint4 a, uint4 b, f4_t c) {
 }
 
 template <bool BF16W>
-__device__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float *smem) {
+__device__ __forceinline__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float *smem) {
     using T = typename MdOps<BF16W>::T;
     using E = typename std::conditional<BF16W, uint16_t, float>::type;
     constexpr int CH = md_ch<BF16W>();
@@ -506,115 +505,267 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
 }
 
 // ------------------------------- fp32 -------------------------------------
-constexpr int F_BK = 64;   // K step: long enough to cover a memory round trip with MFMA work
-constexpr int F_LDA = F_BK + 4;   // padded LDS row (floats)
+// Tiles of BM = 16 * RB rows x 16 hidden units (48 weight rows: the units'
+// reset, update and candidate rows). The row-tile height follows the row
+// count: R row tiles per unit tile, with R chosen so that R x (H / 16) tiles
+// make about one tile per CU, so any M up to 128 * R rows is split into R
+// nearly equal row tiles (16-row granularity) and the CUs stay evenly loaded
+// (at H = 1024: four row tiles of at most 128 rows for M <= 512).
+// The block's 8 waves form 2 row groups x 4 K quarters: wave w takes the row
+// blocks rb = g, g + 2, ... (g = w / 4) and k = 16 (w % 4) .. + 15 of every
+// 64-wide K step. Waves w and w + 4 share a SIMD, so every SIMD carries the
+// same MFMA work whatever RB is, even when the two groups' row-block counts
+// differ. The four K quarters' partial sums meet in LDS in a fixed order, two
+// row blocks at a time, and each thread applies the gates to one output.
+constexpr int KS_TU = 16;            // hidden units per tile
+constexpr int KS_RBMAX = 8;          // 16-row blocks per tile at most
+constexpr int KS_BK = 64;            // K step
+constexpr int KS_LDA = KS_BK + 4;    // padded LDS row (floats)
+constexpr int KS_BROWS = 3 * KS_TU;  // weight rows per tile
+constexpr int KS_OPER = 2 * (16 * KS_RBMAX + KS_BROWS) * KS_LDA;   // two operand buffers (floats)
+constexpr int KS_PTRS = KS_OPER;     // per tile row: destination, history source, input source (u64 each)
+constexpr int KS_HPREV = KS_PTRS + 16 * KS_RBMAX * 6;   // per tile row: h of the tile's 16 units
+static_assert(KS_HPREV + 16 * KS_RBMAX * KS_TU <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
+static_assert(2 * 8 * 4 * 64 * 4 <= KS_OPER, "fp32 partial sums exceed the operand buffers");
 
-__device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
-    const int NJ = d.H / G_BJ;
-    int mt, jt;
-    gru_tile_of(tile, NJ, mt, jt);
-    const int m0 = mt * G_BM, j0 = jt * G_BJ;
-    if (m0 >= M) return;
+typedef float (*KsLds)[16 * KS_RBMAX + KS_BROWS][KS_LDA];
 
-    auto As = reinterpret_cast<float (*)[G_BM][F_LDA]>(smem);
-    auto Bs = reinterpret_cast<float (*)[3 * G_BJ][F_LDA]>(smem + 2 * G_BM * F_LDA);
+// row tiles of the fp32 tiled path for M rows
+__device__ __forceinline__ int ks_row_tiles(const Dev &d, int M) {
+    const int NU = d.H / KS_TU;
+    const int R0 = max(1, 256 / NU);
+    return R0 * ((M + 128 * R0 - 1) / (128 * R0));
+}
+
+// The register stage of one K step: NPA A rows and two B rows per thread.
+template <int NPA>
+struct KsStage {
+    float4 a[NPA], b0, b1;
+};
+
+// Every thread issues the same loads, none behind a branch (a pass past the
+// tile re-reads its last row, and every thread loads a second B row), so
+// that the wait for one stage never has to cover the next one as well.
+template <int RB>
+__device__ __forceinline__ void ks_load(KsStage<(16 * RB + 31) / 32> &S, const u64 *ptrs, int a_r, int a_k, int k0,
+                                        int Kx, const float *bp0, const float *bp1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+    const bool xp = k0 < Kx;   // uniform: a K step lies wholly in the input part or the history part
+#pragma unroll
+    for (int p = 0; p < NPA; ++p) {
+        const int row = min(a_r + 32 * p, BM - 1);
+        const float *src = reinterpret_cast<const float *>(ptrs[3 * row + (xp ? 2 : 1)]);
+        S.a[p] = ldg<float4>(src + (xp ? k0 : k0 - Kx) + a_k);
+    }
+    S.b0 = ldg<float4>(bp0 + k0);
+    S.b1 = ldg<float4>(bp1 + k0);
+}
+
+template <int RB>
+__device__ __forceinline__ void ks_store(const KsStage<(16 * RB + 31) / 32> &S, KsLds As, int buf, int a_r, int a_k,
+                                         bool has_b1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (a_r + 32 * p < BM) *reinterpret_cast<float4 *>(&As[buf][a_r + 32 * p][a_k]) = S.a[p];
+    *reinterpret_cast<float4 *>(&As[buf][BM + a_r][a_k]) = S.b0;
+    if (has_b1) *reinterpret_cast<float4 *>(&As[buf][BM + 32 + a_r][a_k]) = S.b1;
+}
+
+// One K step of a wave of row group G: its row blocks G, G + 2, ... x
+// (reset, update, candidate) over its 16 k of the step, four per MFMA. NG:
+// the candidate gate's accumulator (2: input part, 3: history part).
+template <int RB, int G, int NG>
+__device__ __forceinline__ void ks_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KsLds As, int buf,
+                                        int rl, int kc) {
+    constexpr int NRB = (RB - G + 1) / 2;   // 0 for the second group of a one-block tile
+    if constexpr (NRB == 0) return;
+    float4 a[NRB > 0 ? NRB : 1], b[3];
+#pragma unroll
+    for (int g = 0; g < 3; ++g) b[g] = *reinterpret_cast<const float4 *>(&As[buf][16 * RB + 16 * g + rl][kc]);
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) a[i] = *reinterpret_cast<const float4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int i = 0; i < NRB; ++i) {
+            acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[0][c], acc[i][0], 0, 0, 0);
+            acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[1][c], acc[i][1], 0, 0, 0);
+            acc[i][NG] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[2][c], acc[i][NG], 0, 0, 0);
+        }
+    }
+}
+
+// What the epilogue of a tile needs besides the partial sums.
+struct KsEpi {
+    const u64 *ptrs;     // per tile row: destination (0 past M), history source, input source
+    const float *hprev;  // per tile row: h of the tile's 16 units
+    float br, bz, bn;    // this thread's unit's biases
+    int j;               // this thread's unit
+    size_t lofs;         // this layer's offset in a destination row
+};
+
+// The K loop, the partial sums and the gates, as run by a wave of row group
+// G (wave-uniform). Every wave runs the same barriers whatever its group.
+template <int RB, int G>
+__device__ __forceinline__ void ks_waves(KsLds As, float *smem, const KsEpi &ep, int a_r, int a_k, int Kx, int nk,
+                                         const float *bp0, const float *bp1, bool has_b1, int w, int lane, int tid) {
+    constexpr int NPA = (16 * RB + 31) / 32;
+    constexpr int NRB = (RB - G + 1) / 2;
+    f4_t acc[NRB > 0 ? NRB : 1][4];   // [row block G + 2 i][reset, update, candidate input part, candidate history part]
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) acc[i][g] = f4_t{0, 0, 0, 0};
+    const int rl = lane & 15, kc = 16 * (w & 3) + 4 * (lane >> 4);
+    // two register stages: the loads of step s + 2 are issued while step s
+    // multiplies; S0 carries the odd steps and S1 the even ones from step 2
+    // on, and LDS buffer s & 1 holds step s (step 0 is in LDS already)
+    KsStage<NPA> S0, S1;
+    ks_load<RB>(S0, ep.ptrs, a_r, a_k, KS_BK, Kx, bp0, bp1);
+    ks_load<RB>(S1, ep.ptrs, a_r, a_k, min(2, nk - 1) * KS_BK, Kx, bp0, bp1);
+    // step kt: multiply LDS buffer kt & 1; store the stage holding step kt + 1
+    // into the other buffer and load step kt + 3 into it (S0 holds the odd
+    // steps, S1 the even ones); NG: the candidate gate's accumulator. The
+    // input part's steps come first, then the history part's, each in a loop
+    // of its own, so that no branch between MFMAs picks the accumulator.
+    auto step = [&](int kt, auto NGc, auto PARc) {
+        constexpr int NG = decltype(NGc)::value, PAR = decltype(PARc)::value;
+        ks_step<RB, G, NG>(acc, As, PAR, rl, kc);
+        KsStage<NPA> &St = PAR == 0 ? S0 : S1;
+        if (kt + 1 < nk) ks_store<RB>(St, As, 1 - PAR, a_r, a_k, has_b1);
+        // past the last step the stage re-reads the last step (unused), so
+        // that every step issues the same loads and the waits stay exact
+        ks_load<RB>(St, ep.ptrs, a_r, a_k, min(kt + 3, nk - 1) * KS_BK, Kx, bp0, bp1);
+        __syncthreads();
+    };
+    using X = std::integral_constant<int, 2>;
+    using Hh = std::integral_constant<int, 3>;
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    const int nx = Kx / KS_BK;
+    int kt = 0;
+    for (; kt + 1 < nx; kt += 2) {
+        step(kt, X(), P0());
+        step(kt + 1, X(), P1());
+    }
+    if (kt < nx) step(kt++, X(), P0());
+    if (kt & 1) step(kt++, Hh(), P1());
+    for (; kt + 1 < nk; kt += 2) {
+        step(kt, Hh(), P0());
+        step(kt + 1, Hh(), P1());
+    }
+    if (kt < nk) step(kt, Hh(), P0());
+    // Rounds of two row blocks (2p from group 0, 2p + 1 from group 1): the
+    // waves write their partial sums, [area p & 1][group][K quarter][part]
+    // [lane], over the operand buffers; thread (h, i, u) then sums the four K
+    // quarters of row i, unit u of row block 2p + h in a fixed order and
+    // applies the gates.
+    const float *red = smem;
+    const int h = tid >> 8, ei = (tid >> 4) & 15, eu = tid & 15;
+#pragma unroll
+    for (int p = 0; p < (RB + 1) / 2; ++p) {
+        if (p < NRB) {
+            float4 *r = reinterpret_cast<float4 *>(smem) + (((p & 1) * 2 + G) * 4 + (w & 3)) * (4 * 64);
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                r[g * 64 + lane] = make_float4(acc[p][g][0], acc[p][g][1], acc[p][g][2], acc[p][g][3]);
+        }
+        __syncthreads();
+        const int rb = 2 * p + h;
+        if (rb < RB) {   // wave-uniform
+            // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+            const float *rf = red + ((p & 1) * 2 + h) * (4 * 4 * 256) + (16 * (ei >> 2) + eu) * 4 + (ei & 3);
+            float sg[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) sg[g] += rf[(q * 4 + g) * 256];
+            const int row = 16 * rb + ei;
+            const u64 dp = ep.ptrs[3 * row];
+            if (dp) {
+                const float rr = sigmoidf_(sg[0] + ep.br);
+                const float z = sigmoidf_(sg[1] + ep.bz);
+                const float n = tanhf(sg[2] + ep.bn + rr * sg[3]);
+                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
+            }
+        }
+    }
+}
+
+template <int RB>
+__device__ __forceinline__ void gru_ks_f32(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile, int NR) {
+    constexpr int BM = 16 * RB;
+    constexpr int NPA = (BM + 31) / 32;   // A rows per loading thread
+    const int NU = d.H / KS_TU;
+    int rt, ut;
+    if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles (and their weights in its L2)
+        const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
+        rt = idx / per;
+        ut = xcd + 8 * (idx % per);
+    } else {
+        rt = tile / NU;
+        ut = tile % NU;
+    }
+    const int m0 = rt * BM, j0 = ut * KS_TU;
+    if (rt >= NR || m0 >= M) return;   // block-uniform
+
+    KsLds As = reinterpret_cast<KsLds>(smem);               // rows 0..BM-1: A, then the 48 B rows
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KS_PTRS);   // [BM][3]; the sources point at this layer's part
+    float *hprev = smem + KS_HPREV;                         // [BM][16]
 
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const float *Wp = reinterpret_cast<const float *>(d.Wl);
 
-    // A loader: row tid/8, 4 consecutive k at (tid%8)*4 and 32 further on.
-    // Rows past M load row M - 1 (m0 < M): their products only reach output
-    // rows the epilogue does not write, and no select sits between a load
-    // and its use.
-    const int a_row = tid >> 3, a_k = (tid & 7) * 4;
-    const RowSrc src = row_source(d, R, layer, min(m0 + a_row, M - 1), M);
-    const float *ax = reinterpret_cast<const float *>(src.x), *ah = src.h;
-    // B loader: rows (gate, unit) tid/8 and tid/8 + 64, the same two k chunks
-    const int b_k = (tid & 7) * 4;
-    const int b_r0 = tid >> 3, b_r1 = b_r0 + 64;
-    const float *bp0 = Wp + (size_t)((b_r0 / G_BJ) * d.H + j0 + (b_r0 % G_BJ)) * K + b_k;
-    const float *bp1 = Wp + (size_t)((b_r1 / G_BJ) * d.H + j0 + (b_r1 % G_BJ)) * K + b_k;
-    const bool has_b1 = b_r1 < 3 * G_BJ;
-
-    // Two register stages: the loads of K step s + 2 are issued while step s
-    // multiplies, so each has two steps of MFMA work to arrive in.
-    struct Stage {
-        float4 a[2], b0[2], b1[2];
-    };
-    auto load = [&](Stage &S, int k0) {   // a K step lies wholly in the input part or the history part
-        const float *ap = k0 < Kx ? ax + k0 : ah + (k0 - Kx);   // uniform choice
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            S.a[c] = ldg<float4>(ap + a_k + 32 * c);
-            S.b0[c] = ldg<float4>(bp0 + k0 + 32 * c);
-            if (has_b1) S.b1[c] = ldg<float4>(bp1 + k0 + 32 * c);
-        }
-    };
-    auto store = [&](const Stage &S, int buf) {
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            *reinterpret_cast<float4 *>(&As[buf][a_row][a_k + 32 * c]) = S.a[c];
-            *reinterpret_cast<float4 *>(&Bs[buf][b_r0][b_k + 32 * c]) = S.b0[c];
-            if (has_b1) *reinterpret_cast<float4 *>(&Bs[buf][b_r1][b_k + 32 * c]) = S.b1[c];
-        }
-    };
-
-    f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-    const int rb = w & 3, ub = w >> 2;
-    const int fr = lane & 15, fk = 4 * (lane >> 4);
-    // a step's LDS fragments are all read before its MFMAs, so that their
-    // latency is paid once per step; the candidate gate's accumulator is
-    // chosen once per step (a step lies in one part of K)
-    auto compute = [&](int buf, bool xphase) {
-        float4 a[F_BK / 16], br[F_BK / 16], bz[F_BK / 16], bn[F_BK / 16];
-#pragma unroll
-        for (int hh = 0; hh < F_BK / 16; ++hh) {
-            a[hh] = *reinterpret_cast<const float4 *>(&As[buf][rb * 16 + fr][hh * 16 + fk]);
-            br[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][0 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-            bz[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][1 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-            bn[hh] = *reinterpret_cast<const float4 *>(&Bs[buf][2 * G_BJ + ub * 16 + fr][hh * 16 + fk]);
-        }
-        f4_t an = xphase ? anx : anh;
-#pragma unroll
-        for (int hh = 0; hh < F_BK / 16; ++hh) {
-            const float av[4] = {a[hh].x, a[hh].y, a[hh].z, a[hh].w};
-            const float rv[4] = {br[hh].x, br[hh].y, br[hh].z, br[hh].w};
-            const float zv[4] = {bz[hh].x, bz[hh].y, bz[hh].z, bz[hh].w};
-            const float nv[4] = {bn[hh].x, bn[hh].y, bn[hh].z, bn[hh].w};
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                ar = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], rv[c], ar, 0, 0, 0);
-                az = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], zv[c], az, 0, 0, 0);
-                an = __builtin_amdgcn_mfma_f32_16x16x4f32(av[c], nv[c], an, 0, 0, 0);
-            }
-        }
-        if (xphase) anx = an;
-        else anh = an;
-    };
-
-    // S0 carries the odd steps and S1 the even ones from step 2 on; LDS buffer
-    // s & 1 holds step s
-    const int nk = K / F_BK;   // >= 2: E, H are multiples of 64
-    Stage S0, S1;
-    load(S0, 0);
-    store(S0, 0);
-    load(S0, F_BK);
-    if (nk > 2) load(S1, 2 * F_BK);
-    __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-        compute(0, kt * F_BK < Kx);
-        if (kt + 1 < nk) store(S0, 1);
-        if (kt + 3 < nk) load(S0, (kt + 3) * F_BK);
-        __syncthreads();
-        if (kt + 1 >= nk) break;
-        compute(1, (kt + 1) * F_BK < Kx);
-        if (kt + 2 < nk) store(S1, 0);
-        if (kt + 4 < nk) load(S1, (kt + 4) * F_BK);
-        __syncthreads();
+    // the tile's row pointers: destination (0 past M), history source and
+    // input source; rows past M read row M - 1 (their products only reach
+    // rows the epilogue skips, and no select sits between a load and its use)
+    if (tid < BM) {
+        const int m = min(m0 + tid, M - 1);
+        const RowSrc src = row_source(d, R, layer, m, M);
+        ptrs[3 * tid] = m0 + tid < M ? (u64)row_at(R, d.f_rowdst, m) : 0;
+        ptrs[3 * tid + 1] = (u64)src.h;
+        ptrs[3 * tid + 2] = (u64)src.x;
     }
-    gru_epilogue(d, R, layer, M, m0, j0, rb, ub, ar, az, anx, anh);
+    __syncthreads();
+    // A loader: rows tid/16 + 32 p, 4 consecutive k at 4 (tid % 16). B
+    // loader: weight rows tid/16 (and tid/16 + 32 for tid < 256): gate
+    // row / 16, unit row % 16
+    const int a_r = tid >> 4, a_k = (tid & 15) * 4;
+    const float *bp0 = Wp + (size_t)((a_r >> 4) * d.H + j0 + (a_r & 15)) * K + a_k;
+    const float *bp1 = Wp + (size_t)(2 * d.H + j0 + (a_r & 15)) * K + a_k;
+    const bool has_b1 = tid < 256;   // wave-uniform
+
+    // step 0 into LDS, with the epilogue's h (the tile's 16 units of each
+    // row's history): thread (row i, unit u) for rows i = tid/16 + 32 p
+    const int hi = tid >> 4, hu = tid & 15;
+    float hv[NPA];
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hv[p] = reinterpret_cast<const float *>(ptrs[3 * (hi + 32 * p) + 1])[j0 + hu];
+    KsEpi ep;
+    ep.ptrs = ptrs;
+    ep.hprev = hprev;
+    ep.j = j0 + hu;
+    ep.br = d.bl[ep.j];
+    ep.bz = d.bl[d.H + ep.j];
+    ep.bn = d.bl[2 * d.H + ep.j];
+    ep.lofs = (size_t)layer * d.H;
+    {
+        KsStage<NPA> S;
+        ks_load<RB>(S, ptrs, a_r, a_k, 0, Kx, bp0, bp1);
+        ks_store<RB>(S, As, 0, a_r, a_k, has_b1);
+    }
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hprev[(hi + 32 * p) * KS_TU + hu] = hv[p];
+    __syncthreads();
+    const int nk = K / KS_BK;   // >= 2: E, H are multiples of 64
+    if (w < 4) ks_waves<RB, 0>(As, smem, ep, a_r, a_k, Kx, nk, bp0, bp1, has_b1, w, lane, tid);
+    else ks_waves<RB, 1>(As, smem, ep, a_r, a_k, Kx, nk, bp0, bp1, has_b1, w, lane, tid);
+    __syncthreads();   // LDS is reused by the next tile
 }
 
 // ------------------------------- bf16 -------------------------------------
@@ -629,7 +780,7 @@ __device__ void gru_mfma_f32(const Dev &d, const Rows &R, int layer, int M, floa
 constexpr int W_BJ = 64, W_BK = 64, W_LDA = W_BK + 8;
 static_assert((2 * G_BM * W_LDA + 2 * 3 * W_BJ * W_LDA) / 2 <= G_LDS_FLOATS, "wide bf16 tiles exceed the LDS buffer");
 
-__device__ void gru_mfma_bf16w(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
+__device__ __forceinline__ void gru_mfma_bf16w(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
     const int NJ = d.H / W_BJ;
     int mt, jt;
     gru_tile_of(tile, NJ, mt, jt);
@@ -734,7 +885,6 @@ __device__ void gru_mfma_bf16w(const Dev &d, const Rows &R, int layer, int M, fl
 }
 
 // One launch per layer; the device-side row count picks the path.
-static_assert(2 * G_BM * F_LDA + 2 * 3 * G_BJ * F_LDA <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
 static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles exceed the LDS buffer");
 static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
 
@@ -787,11 +937,24 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
         gru_medium<BF16W>(d, R, layer, M, smem);
-    } else {                          // 64 x 32 (fp32) or 64 x 64 (bf16) MFMA tiles through LDS
-        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / (BF16W ? W_BJ : G_BJ));
+    } else if (BF16W) {               // 64 x 64 bf16 MFMA tiles through LDS
+        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / W_BJ);
+        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) gru_mfma_bf16w(d, R, layer, M, smem, t);
+    } else {                          // (16 RB) x 16-unit fp32 tiles, K split over the waves
+        const int NR = ks_row_tiles(d, M);
+        const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
+        const int ntiles = NR * (d.H / KS_TU);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
-            if (BF16W) gru_mfma_bf16w(d, R, layer, M, smem, t);
-            else gru_mfma_f32(d, R, layer, M, smem, t);
+            switch (RB) {
+                case 1: gru_ks_f32<1>(d, R, layer, M, smem, t, NR); break;
+                case 2: gru_ks_f32<2>(d, R, layer, M, smem, t, NR); break;
+                case 3: gru_ks_f32<3>(d, R, layer, M, smem, t, NR); break;
+                case 4: gru_ks_f32<4>(d, R, layer, M, smem, t, NR); break;
+                case 5: gru_ks_f32<5>(d, R, layer, M, smem, t, NR); break;
+                case 6: gru_ks_f32<6>(d, R, layer, M, smem, t, NR); break;
+                case 7: gru_ks_f32<7>(d, R, layer, M, smem, t, NR); break;
+                default: gru_ks_f32<8>(d, R, layer, M, smem, t, NR); break;
+            }
         }
     }
 }

@@ -29,9 +29,12 @@ def test_medium_three_digits_prefix():
     assert st["hist_hits"] > 0
 
 
-@pytest.mark.parametrize("qmode,k", [(Q_SIGN, 0), (Q_SIGDIG, 2)])
-def test_large_fp32_prefix(qmode, k):
-    p = make_pair("large", qmode, k, n_frames=6)
+@pytest.mark.parametrize("qmode,k,n", [(Q_SIGN, 0, 6), (Q_SIGDIG, 2, 6), (Q_SIGDIG, 1, 4)],
+                         ids=["sign", "sigdig2", "sigdig1"])
+def test_large_fp32_prefix(qmode, k, n):
+    """Large fp32 frames end to end; sign and 2 digits are the config's runs,
+    1 digit the coarsest decimal row of Table 1 (Sec. 3)."""
+    p = make_pair("large", qmode, k, n_frames=n)
     st = run_frames(p, log_every=1)
     assert st["score_hits"] > 0      # 30% of each frame repeats the previous frame's pairs
 
