@@ -19,7 +19,9 @@
  * stated otherwise. Weights are borrowed and must outlive the context. The
  * library allocates no device memory of its own: packed weights, caches and
  * per-frame scratch live in the caller's workspace (rnnlm_workspace_size).
- * The context object itself is a small host allocation.
+ * The context object itself is a small host allocation. The one exception is
+ * a 4 MiB static device array per GPU, the scratch of the allocation-free
+ * rnnlm_log_normalizer_static.
  *
  * Streams: `stream` arguments are hipStream_t values passed as void* (NULL =
  * the default stream). All work is enqueued on that stream and nothing blocks
@@ -184,6 +186,22 @@ int rnnlm_log_normalizer(rnnlm_t *ctx, const float *h_top, int32_t n, float *log
  * errors as rnnlm_log_normalizer. */
 int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, const int32_t *words, int32_t n, float *logz,
                                 void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * normaliser of rnnlm_log_normalizer without a context or workspace,
+ *   logz[i] = log sum_v exp(U_out[v] . h_top[i] + b_out[v]),  i < n,
+ * computed by the same kernels. U_out: [V][H] fp32, b_out: [V] fp32, h_top:
+ * [n][H] fp32, logz: [n] fp32, all device memory owned by the caller; h_top
+ * and U_out 16-byte aligned; H a multiple of 64, at most 2048; any n >= 0.
+ * The partial (max, sum) pairs live in a static device array of the library
+ * (4 MiB, one per GPU, held until the process ends), so V is at most 425,984;
+ * a larger V, a bad H or a null pointer returns RNNLM_EINVAL before anything
+ * is enqueued. The call allocates nothing and issues no memset: two kernel
+ * launches per 256 rows on `stream`. Calls that overlap on one GPU (other
+ * streams, other host threads) share that array and race; order them. */
+int rnnlm_log_normalizer_static(const float *U_out, const float *b_out, int32_t V, int32_t H,
+                                const float *h_top, int32_t n, float *logz, void *stream);
 
 /* Copy the device statistics, summed over all sessions, into *stats (host
  * memory); synchronises `stream`. Returns RNNLM_EDEVICE if the sticky device

@@ -408,6 +408,36 @@ RNNLM_API int rnnlm_log_normalizer_maxent(rnnlm_t *ctx, const float *h_top, cons
     return log_normalizer(ctx, h_top, words, n, logz, stream, "rnnlm_log_normalizer_maxent launch");
 }
 
+RNNLM_API int rnnlm_log_normalizer_static(const float *U_out, const float *b_out, int32_t V, int32_t H,
+                                          const float *h_top, int32_t n, float *logz, void *stream) {
+    if (V < 1 || rn::lognorm_tiles(V) > rn::kStaticMaxTiles)
+        return fail(RNNLM_EINVAL, "V %d outside [1, %d]: the static scratch holds %d vocabulary tiles", V,
+                    rn::kStaticMaxV, rn::kStaticMaxTiles);
+    if (H < 64 || H % 64 || H > rn::kMaxLH) return fail(RNNLM_EINVAL, "H must be a multiple of 64 in [64, %d]", rn::kMaxLH);
+    if (n < 0) return fail(RNNLM_EINVAL, "n %d < 0", n);
+    if (n == 0) return RNNLM_OK;
+    if (!U_out || !b_out || !h_top || !logz) return fail(RNNLM_EINVAL, "null U_out, b_out, h_top or logz");
+    if ((reinterpret_cast<uintptr_t>(h_top) | reinterpret_cast<uintptr_t>(U_out)) & 15)
+        return fail(RNNLM_EINVAL, "h_top and U_out must be 16-byte aligned");
+    float2 *part = nullptr;
+    hipError_t e = rn::lognorm_static_scratch(&part);
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_log_normalizer_static scratch");
+    rn::Dev d;
+    memset(&d, 0, sizeof d);
+    d.V = V; d.H = H; d.U_out = U_out; d.b_out = b_out;
+    d.me_log2 = 1; d.me_order = 1;   // no MaxEnt terms
+    d.ln_part = part;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    for (int r0 = 0; r0 < n; r0 += 256) {   // each chunk's pairs are combined before the next overwrites them
+        const int nr = n - r0 < 256 ? n - r0 : 256;
+        rn::launch_lognorm_gemm(d, h_top + (size_t)r0 * H, nullptr, nr, s);
+        rn::launch_lognorm_combine(d, nr, logz + r0, s);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "rnnlm_log_normalizer_static launch");
+    return RNNLM_OK;
+}
+
 // Fold every session's pending scoring counts, then read all counters and
 // error words (synchronises).
 static int read_counters(rnnlm_t *ctx, long long (*c)[rn::C_N], unsigned *derr, hipStream_t s) {

@@ -37,6 +37,13 @@ void launch_pack_layer(const Dev &d, int layer, const void *W_ih, const void *W_
 
 
 int lognorm_tiles(int V);
+// The allocation-free normaliser keeps its partial pairs in a static device
+// array sized for kStaticMaxTiles vocabulary tiles (256 rows per launch);
+// its address on the current device (looked up once per device).
+constexpr int kStaticMaxTiles = 2048;
+constexpr int kStaticMaxV = kStaticMaxTiles * 208;   // vocabulary tiles of 208 words
+constexpr int kMaxDevices = 64;
+hipError_t lognorm_static_scratch(float2 **ptr);
 // words: optional [n][3] context words; when given, the MaxEnt weights of
 // every vocabulary word after each row's context join its logit
 void launch_lognorm_gemm(const Dev &d, const float *h, const int32_t *words, int n, hipStream_t s, Stamp ts = {});

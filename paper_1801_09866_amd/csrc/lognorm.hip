@@ -7,6 +7,8 @@
 // 256 rows of h and 128 vocabulary rows, and its epilogue reduces its logits
 // to a (max, sum exp(. - max)) pair per row. No logit reaches HBM.
 // Pass 2: per row, a fixed-shape tree combines the pairs of all tiles.
+#include <mutex>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -24,6 +26,7 @@ static_assert(LN_BK == 16 && LN_BM == 256 && LN_BN > 128 && LN_BN <= 256,
               "loaders: 4 threads x 4 k per row, rows tid / 4 + 128 j");
 
 int lognorm_tiles(int V) { return (V + LN_BN - 1) / LN_BN; }
+static_assert(kStaticMaxV == kStaticMaxTiles * LN_BN, "static normaliser limit");
 
 __global__ __launch_bounds__(512) void k_lognorm_gemm(Dev d, const float *h, const int32_t *words, int n) {
     __shared__ float As[2][LN_BM][LN_LD];
@@ -177,6 +180,31 @@ __global__ __launch_bounds__(256) void k_lognorm_combine(Dev d, int NT, float *l
         __syncthreads();
     }
     if (tid == 0) logz[row] = s[0].x + logf(s[0].y);
+}
+
+// The normaliser's partial pairs for callers that cannot allocate: a
+// file-scope device array, one per GPU, held until the process ends. Host
+// code reaches it only through the address hipGetSymbolAddress returns for
+// the current device (looked up once per device and kept).
+constexpr size_t kStaticPartBytes = size_t(256) * kStaticMaxTiles * sizeof(float2);
+static __device__ __align__(256) float2 scratch[kStaticPartBytes / sizeof(float2)];
+
+hipError_t lognorm_static_scratch(float2 **ptr) {
+    static std::mutex mu;
+    static float2 *by_dev[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!by_dev[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        by_dev[dev] = static_cast<float2 *>(p);
+    }
+    *ptr = by_dev[dev];
+    return hipSuccess;
 }
 
 void launch_lognorm_gemm(const Dev &d, const float *h, const int32_t *words, int n, hipStream_t s, Stamp ts) {

@@ -60,7 +60,8 @@ class Stats(ctypes.Structure):
 
 
 EXPORTS = ("rnnlm_workspace_size", "rnnlm_create", "rnnlm_score_frame", "rnnlm_score_frames",
-           "rnnlm_cache_reset", "rnnlm_log_normalizer", "rnnlm_log_normalizer_maxent", "rnnlm_get_stats",
+           "rnnlm_cache_reset", "rnnlm_log_normalizer", "rnnlm_log_normalizer_maxent",
+           "rnnlm_log_normalizer_static", "rnnlm_get_stats",
            "rnnlm_get_session_stats", "rnnlm_debug_quantize", "rnnlm_profile", "rnnlm_profile_read",
            "rnnlm_destroy", "rnnlm_last_error")
 NSTAGES = 10
@@ -87,6 +88,7 @@ def load(path=LIB_PATH):
     L.rnnlm_cache_reset.argtypes = [c_vp, c_vp]
     L.rnnlm_log_normalizer.argtypes = [c_vp, c_vp, c_i32, c_vp, c_vp]
     L.rnnlm_log_normalizer_maxent.argtypes = [c_vp, c_vp, c_vp, c_i32, c_vp, c_vp]
+    L.rnnlm_log_normalizer_static.argtypes = [c_vp, c_vp, c_i32, c_i32, c_vp, c_i32, c_vp, c_vp]
     L.rnnlm_get_stats.argtypes = [c_vp, P(Stats), c_vp]
     L.rnnlm_debug_quantize.argtypes = [c_i32, c_i32, c_vp, c_i64, c_vp, c_vp, c_vp]
     L.rnnlm_profile.argtypes = [c_vp, ctypes.c_uint32]
@@ -299,6 +301,19 @@ class Scorer:
             self.close()
         except Exception:
             pass
+
+
+def log_normalizer_static(U_out, b_out, h_top, out=None, stream=None):
+    """Full-vocabulary log normaliser without a context or workspace
+    (rnnlm_log_normalizer_static): U_out [V, H], b_out [V], h_top [n, H],
+    fp32 device tensors; the library's static scratch holds the partials."""
+    V, H = int(U_out.shape[0]), int(U_out.shape[1])
+    n = int(h_top.shape[0])
+    if out is None:
+        out = torch.empty(max(n, 1), dtype=torch.float32, device=h_top.device)
+    _check(load().rnnlm_log_normalizer_static(_ptr(U_out), _ptr(b_out), V, H, _ptr(h_top), n, _ptr(out),
+                                              _stream(stream)))
+    return out[:n]
 
 
 def debug_quantize(x, qmode, qdigits=0, stream=None):

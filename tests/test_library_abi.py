@@ -71,6 +71,13 @@ def test_host_argument_checks_need_no_gpu(lib):
     assert lib.rnnlm_debug_quantize(9, 0, None, 64, None, None, None) == R.EINVAL
     assert lib.rnnlm_debug_quantize(R.Q_SIGN, 0, None, 63, None, None, None) == R.EINVAL
     assert lib.rnnlm_debug_quantize(R.Q_SIGN, 0, None, 0, None, None, None) == R.OK
+    # the allocation-free normaliser checks its sizes before touching a device
+    one = ctypes.c_void_p(256)
+    assert lib.rnnlm_log_normalizer_static(one, one, 425_985, 64, one, 4, one, None) == R.EINVAL
+    assert b"425984" in lib.rnnlm_last_error()
+    assert lib.rnnlm_log_normalizer_static(one, one, 1000, 96, one, 4, one, None) == R.EINVAL
+    assert lib.rnnlm_log_normalizer_static(None, one, 1000, 64, one, 4, one, None) == R.EINVAL
+    assert lib.rnnlm_log_normalizer_static(one, one, 1000, 64, one, 0, one, None) == R.OK
 
 
 def test_sessions_scale_the_per_session_state(lib):
