@@ -210,6 +210,10 @@ size_t layout(const rnnlm_config &c, char *base, rn::Dev &d, void **packed) {
     d.f_rowh = cv.take<unsigned long long>(mh);
     d.f_rowdst = cv.take<unsigned long long>(mh);
     d.f_hval = cv.take<float>(mh * LH);
+    const bool bf = c.wdtype == RNNLM_BF16;
+    d.f_hbf = cv.take<uint16_t>(bf ? mh * LH : 8);
+    d.f_rowhb = cv.take<unsigned long long>(mh);
+    d.f_xbf = cv.take<uint16_t>(bf && c.L == 2 ? mh * c.H : 8);
     d.f_qkey = cv.take<int4>(mq);
     d.f_qwords = cv.take<int4>(mq);
     d.f_qrec = cv.take<rn::QRec>(mq);

@@ -125,6 +125,10 @@ struct Dev {
     u64 *f_rowh;      // address of row r's history vector (all layers)
     u64 *f_rowdst;    // where row r writes its h'
     float *f_hval;    // [max_hist][LH] h' of rows the cache did not admit
+    // bf16 weights: the GEMM's A operand, rounded to bf16 once per frame
+    uint16_t *f_hbf;  // [max_hist][LH] each history row (written by the keys kernel)
+    u64 *f_rowhb;     // address of row r's bf16 history row
+    uint16_t *f_xbf;  // two layers: [max_hist][H] the first layer's h' of row r (its tiles' epilogue)
     // per-frame query scratch
     int4 *f_qkey;     // (history index, w-2, w-3, target) for exact key checks
     int4 *f_qwords;   // (w-1, w-2, w-3, target) of each query, as the scorer reads them
@@ -163,6 +167,9 @@ __host__ __device__ __forceinline__ Dev session_view(const Dev &d0, int s) {
     d.f_rowh = shift_ptr(d.f_rowh, o);
     d.f_rowdst = shift_ptr(d.f_rowdst, o);
     d.f_hval = shift_ptr(d.f_hval, o);
+    d.f_hbf = shift_ptr(d.f_hbf, o);
+    d.f_rowhb = shift_ptr(d.f_rowhb, o);
+    d.f_xbf = shift_ptr(d.f_xbf, o);
     d.f_qkey = shift_ptr(d.f_qkey, o);
     d.f_qwords = shift_ptr(d.f_qwords, o);
     d.f_qrec = shift_ptr(d.f_qrec, o);
@@ -212,6 +219,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     uint32_t u = __float_as_uint(f);
     u += 0x7FFFu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
+}
+
+// four fp32 as four bf16 (RNE), lowest element in the lowest half-word
+__device__ __forceinline__ uint2 pack_bf16x4(float4 a) {
+    uint2 r;
+    r.x = (uint32_t)f32_to_bf16(a.x) | ((uint32_t)f32_to_bf16(a.y) << 16);
+    r.y = (uint32_t)f32_to_bf16(a.z) | ((uint32_t)f32_to_bf16(a.w) << 16);
+    return r;
 }
 
 // A history handle is bad when null or not 16-byte aligned.

@@ -170,7 +170,7 @@ __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
 }
 
 // One LDS buffer serves every path.
-constexpr int G_LDS_FLOATS = 27648;   // 108 KB
+constexpr int G_LDS_FLOATS = 35840;   // 140 KB
 
 // ------------------------ medium path (32 < rows <= 256) -------------------
 // Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
@@ -769,119 +769,235 @@ __device__ __forceinline__ void gru_ks_f32(const Dev &d, const Rows &R, int laye
 }
 
 // ------------------------------- bf16 -------------------------------------
-// A bf16 K step is little MFMA work for the bytes it loads, so this tile is
-// bound by the bytes it has in flight rather than by the matrix units. fp32
-// operand rows stay fp32 in the register stage and are rounded to bf16 when
-// written to LDS, so that no arithmetic waits on a load before its step.
-// bf16 tile of 64 rows x 64 hidden units (three gates: 192 weight rows),
-// 64-wide K steps, two register stages. Against the 64 x 32 tile it reads
-// each operand row half as often and moves fewer bytes per MFMA; each wave
-// owns 16 rows and two 16-unit blocks.
-constexpr int W_BJ = 64, W_BK = 64, W_LDA = W_BK + 8;
-static_assert((2 * G_BM * W_LDA + 2 * 3 * W_BJ * W_LDA) / 2 <= G_LDS_FLOATS, "wide bf16 tiles exceed the LDS buffer");
+// Tiles of 128 rows x 32 hidden units (96 weight rows), K in steps of 128
+// through double-buffered LDS, all operands bf16: the history rows were
+// rounded once per frame by the keys kernel, and the second layer's input is
+// the bf16 copy of the first layer's h' that its tiles' epilogue writes, so a
+// tile moves 2 bytes per operand element and converts nothing. The 8 waves
+// are 4 row groups x 2 K halves: wave w takes the row blocks g and g + 4
+// (g = w % 4) and k = 64 (w / 4) .. + 63 of every step, 32 k per
+// 16 x 16 x 32 MFMA; waves w and w + 4 share a SIMD and the same rows. The two
+// K halves' partial sums meet in LDS (in a fixed order) and the first half's
+// waves apply the gates.
+constexpr int KB_BM = 128, KB_TU = 32, KB_BK = 128, KB_LDA = KB_BK + 8;   // LDA in bf16
+constexpr int KB_ROWS = KB_BM + 3 * KB_TU;                                // A rows, then the weight rows
+constexpr int KB_OPER = 2 * KB_ROWS * KB_LDA / 2;                         // two operand buffers (floats)
+constexpr int KB_PTRS = KB_OPER;                                          // [128][5] u64 per tile row
+constexpr int KB_HPREV = KB_PTRS + KB_BM * 10;                            // [128][32] fp32 h
+static_assert(KB_HPREV + KB_BM * KB_TU <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
+static_assert(4 * 16 * 64 * 4 <= KB_OPER, "bf16 partial sums exceed the operand buffers");
 
-__device__ __forceinline__ void gru_mfma_bf16w(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
-    const int NJ = d.H / W_BJ;
+// address of element `idx` of row m of a per-session per-row array of `stride` elements
+template <class T>
+__device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t stride) {
+    long long o = R.sofs[0];
+    int base = 0;
+    if (R.n > 1) {   // uniform
+#pragma unroll
+        for (int e = 1; e < kMaxSessions; ++e)
+            if (e < R.n && m >= R.moff[e]) {
+                o = R.sofs[e];
+                base = R.moff[e];
+            }
+    }
+    return shift_ptr(arr, o) + (size_t)(m - base) * stride;
+}
+
+// The register stage of one K step: 4 A chunks and 3 weight chunks of 8
+// bf16 per thread (thread t: rows t/16 + 32 j, chunk t % 16).
+struct KbStage {
+    uint4 v[7];
+};
+
+// One K step of a wave: per 32-k depth, its two row blocks x two unit blocks
+// x (reset, update, candidate input part, candidate history part). The
+// candidate gate's weight fragment feeds both of its accumulators, with zeros
+// in place of the part the depth does not lie in (and every fragment zero for
+// a depth past K), so that one branch-free instruction stream serves every
+// step; the extra MFMAs are cheap next to the bytes a bf16 step moves.
+__device__ __forceinline__ void kb_mfma(f4_t (&acc)[2][2][4], const uint16_t (*As)[KB_LDA], int rg, int kh, int lane,
+                                        int k0, int Kx, int K) {
+    const int fr = lane & 15, fk = 8 * (lane >> 4);
+#pragma unroll
+    for (int kd = 0; kd < 2; ++kd) {
+        const int kr = 64 * kh + 32 * kd;   // wave-uniform
+        const bool live = k0 + kr < K, xp = k0 + kr < Kx;
+        const uint4 z = make_uint4(0, 0, 0, 0);
+        bf8_t a[2], b[2][4];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(&As[16 * (rg + 4 * i) + fr][kr + fk]);
+            a[i] = __builtin_bit_cast(bf8_t, live ? v : z);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            uint4 g[3];
+#pragma unroll
+            for (int q = 0; q < 3; ++q)
+                g[q] = *reinterpret_cast<const uint4 *>(&As[KB_BM + q * KB_TU + 16 * u + fr][kr + fk]);
+            b[u][0] = __builtin_bit_cast(bf8_t, g[0]);
+            b[u][1] = __builtin_bit_cast(bf8_t, g[1]);
+            b[u][2] = __builtin_bit_cast(bf8_t, xp ? g[2] : z);
+            b[u][3] = __builtin_bit_cast(bf8_t, xp ? z : g[2]);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    acc[i][u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[u][q], acc[i][u][q], 0, 0, 0);
+    }
+}
+
+__device__ __forceinline__ void gru_kb_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
+    const int NU = d.H / KB_TU;
     int mt, jt;
-    gru_tile_of(tile, NJ, mt, jt);
-    const int m0 = mt * G_BM, j0 = jt * W_BJ;
-    if (m0 >= M) return;
+    gru_tile_of(tile, NU, mt, jt);
+    const int m0 = mt * KB_BM, j0 = jt * KB_TU;
+    if (m0 >= M) return;   // block-uniform
 
-    uint16_t *sm16 = reinterpret_cast<uint16_t *>(smem);
-    auto As = reinterpret_cast<uint16_t (*)[G_BM][W_LDA]>(sm16);
-    auto Bs = reinterpret_cast<uint16_t (*)[3 * W_BJ][W_LDA]>(sm16 + 2 * G_BM * W_LDA);
-
+    auto As = reinterpret_cast<uint16_t (*)[KB_ROWS][KB_LDA]>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KB_PTRS);   // per row: dst, h fp32, h bf16, x bf16, x copy dst
+    float *hprev = smem + KB_HPREV;
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
 
-    // A: row tid/8, 8 elements at (tid%8)*8; rows past M read row M - 1
-    const int a_row = tid >> 3, a_k = (tid & 7) * 8;
-    const RowSrc src = row_source(d, R, layer, min(m0 + a_row, M - 1), M);
-    // B: weight rows tid/8 + 64c (c < 3: one per gate), same 8 elements
+    // the tile's row pointers (rows past M read row M - 1: their products
+    // only reach rows the epilogue skips)
+    if (tid < KB_BM) {
+        const int m = min(m0 + tid, M - 1);
+        const bool live = m0 + tid < M;
+        ptrs[5 * tid] = live ? row_at(R, d.f_rowdst, m) : 0;
+        ptrs[5 * tid + 1] = row_at(R, d.f_rowh, m) + (u64)layer * d.H * 4;
+        ptrs[5 * tid + 2] = row_at(R, d.f_rowhb, m) + (u64)layer * d.H * 2;
+        ptrs[5 * tid + 3] = layer == 0 ? (u64)(reinterpret_cast<const uint16_t *>(d.emb) +
+                                               (size_t)(unsigned)row_at(R, d.f_roww, m) * d.E)
+                                       : (u64)row_ptr(R, d.f_xbf, m, d.H);
+        ptrs[5 * tid + 4] = live && layer == 0 && d.L == 2 ? (u64)row_ptr(R, d.f_xbf, m, d.H) : 0;
+    }
+    __syncthreads();
+    // the epilogue's fp32 h: thread t, unit t % 32, rows t / 32 + 16 j
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+        const int r = (tid >> 5) + 16 * jj;
+        hprev[r * KB_TU + (tid & 31)] = reinterpret_cast<const float *>(ptrs[5 * r + 1])[j0 + (tid & 31)];
+    }
+    // loaders: thread t, chunk t % 16 (8 k) of A rows t/16 + 32 j (j < 4) and
+    // weight rows t/16 + 32 j (j < 3): gate row / 32, unit row % 32
+    const int lr = tid >> 4, lc = (tid & 15) * 8;
     const uint16_t *bp[3];
 #pragma unroll
-    for (int c = 0; c < 3; ++c) bp[c] = Wp + (size_t)(c * d.H + j0 + (tid >> 3)) * K + a_k;
-
-    struct Stage {
-        float4 a[2];   // fp32 source; a bf16 source keeps its 8 elements in a[0]
-        uint4 b[3];
-    };
-    auto load = [&](Stage &S, int k0) {   // a K step lies wholly in the input part or the history part
-        if (k0 < Kx && src.x_bf16) {      // uniform
-            S.a[0] = __builtin_bit_cast(float4, ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k0 + a_k));
-        } else {
-            const float *p = (k0 < Kx ? reinterpret_cast<const float *>(src.x) + k0 : src.h + (k0 - Kx)) + a_k;
-            S.a[0] = ldg<float4>(p);
-            S.a[1] = ldg<float4>(p + 4);
-        }
-#pragma unroll
-        for (int c = 0; c < 3; ++c) S.b[c] = ldg<uint4>(bp[c] + k0);
-    };
-    auto store = [&](const Stage &S, int buf, int k0) {
-        const bool raw16 = k0 < Kx && src.x_bf16;   // uniform
-        *reinterpret_cast<uint4 *>(&As[buf][a_row][a_k]) =
-            raw16 ? __builtin_bit_cast(uint4, S.a[0]) : pack_bf16x8(S.a[0], S.a[1]);
-#pragma unroll
-        for (int c = 0; c < 3; ++c) *reinterpret_cast<uint4 *>(&Bs[buf][64 * c + (tid >> 3)][a_k]) = S.b[c];
-    };
-
-    f4_t acc[2][4];   // [unit block][r, z, n input part, n history part]
-#pragma unroll
-    for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) acc[q][g] = f4_t{0, 0, 0, 0};
-    const int rb = w & 3, ub = w >> 2;   // unit blocks ub and ub + 2
-    const int fr = lane & 15, fk = 8 * (lane >> 4);
-    auto compute = [&](int buf, bool xphase) {
-        bf8_t a[2], b[2][2][3];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-            a[hh] = *reinterpret_cast<const bf8_t *>(&As[buf][rb * 16 + fr][hh * 32 + fk]);
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-                for (int g = 0; g < 3; ++g)
-                    b[hh][q][g] = *reinterpret_cast<const bf8_t *>(&Bs[buf][g * W_BJ + (ub + 2 * q) * 16 + fr][hh * 32 + fk]);
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-            f4_t an = xphase ? acc[q][2] : acc[q][3];
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh) {
-                acc[q][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][0], acc[q][0], 0, 0, 0);
-                acc[q][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][1], acc[q][1], 0, 0, 0);
-                an = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hh], b[hh][q][2], an, 0, 0, 0);
-            }
-            if (xphase) acc[q][2] = an;
-            else acc[q][3] = an;
-        }
-    };
-
-    // S0 carries the odd steps and S1 the even ones from step 2 on; LDS buffer
-    // s & 1 holds step s
-    const int nk = K / W_BK;   // >= 2
-    Stage S0, S1;
-    load(S0, 0);
-    store(S0, 0, 0);
-    load(S0, W_BK);
-    if (nk > 2) load(S1, 2 * W_BK);
-    __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-        compute(0, kt * W_BK < Kx);
-        if (kt + 1 < nk) store(S0, 1, (kt + 1) * W_BK);
-        if (kt + 3 < nk) load(S0, (kt + 3) * W_BK);
-        __syncthreads();
-        if (kt + 1 >= nk) break;
-        compute(1, (kt + 1) * W_BK < Kx);
-        if (kt + 2 < nk) store(S1, 0, (kt + 2) * W_BK);
-        if (kt + 4 < nk) load(S1, (kt + 4) * W_BK);
-        __syncthreads();
+    for (int j = 0; j < 3; ++j) {
+        const int br = lr + 32 * j;
+        bp[j] = Wp + (size_t)((br >> 5) * d.H + j0 + (br & 31)) * K;
     }
+    auto load = [&](KbStage &S, int k0) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
-        gru_epilogue(d, R, layer, M, m0, j0, rb, ub + 2 * q, acc[q][0], acc[q][1], acc[q][2], acc[q][3]);
+        for (int j = 0; j < 4; ++j) {
+            const u64 *pr = ptrs + 5 * (lr + 32 * j);
+            const int k = min(k0 + lc, K - 8);   // past K: an unused chunk, in bounds
+            const uint16_t *src = k < Kx ? reinterpret_cast<const uint16_t *>(pr[3]) + k
+                                         : reinterpret_cast<const uint16_t *>(pr[2]) + (k - Kx);
+            S.v[j] = ldg<uint4>(src);
+        }
+#pragma unroll
+        for (int j = 0; j < 3; ++j) S.v[4 + j] = ldg<uint4>(bp[j] + min(k0 + lc, K - 8));
+    };
+    auto store = [&](const KbStage &S, int buf) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4 *>(&As[buf][lr + 32 * j][lc]) = S.v[j];
+#pragma unroll
+        for (int j = 0; j < 3; ++j) *reinterpret_cast<uint4 *>(&As[buf][KB_BM + lr + 32 * j][lc]) = S.v[4 + j];
+    };
+
+    const int rg = w & 3, kh = w >> 2;
+    f4_t acc[2][2][4];   // [row block rg + 4 i][unit block][reset, update, candidate input part, history part]
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc[i][u][g] = f4_t{0, 0, 0, 0};
+    // epilogue operands of the first K half's lanes: biases of their two units
+    float bias[2][3];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int g = 0; g < 3; ++g) bias[u][g] = kh == 0 ? d.bl[g * d.H + j0 + 16 * u + (lane & 15)] : 0.f;
+
+    // two register stages: the loads of step s + 2 are issued while step s
+    // multiplies; LDS buffer s & 1 holds step s
+    const int ns = (K + KB_BK - 1) / KB_BK;   // steps (the last may reach past K by 64)
+    KbStage S0, S1;
+    load(S0, 0);
+    store(S0, 0);
+    load(S0, KB_BK);
+    load(S1, 2 * KB_BK);
+    __syncthreads();
+    // step s multiplies buffer s & 1, stores step s + 1 (held by S0 for even
+    // s, S1 for odd s) into the other buffer and loads step s + 3 into it
+    // (past the last step: an unused reload of the last step, so that every
+    // step issues the same loads and the waits stay exact)
+    auto step = [&](int st, auto PARc) {
+        constexpr int PAR = decltype(PARc)::value;
+        kb_mfma(acc, As[PAR], rg, kh, lane, st * KB_BK, Kx, K);
+        KbStage &S = PAR == 0 ? S0 : S1;
+        if (st + 1 < ns) store(S, 1 - PAR);
+        load(S, min(st + 3, ns - 1) * KB_BK);
+        __syncthreads();
+    };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    int st = 0;
+    for (; st + 1 < ns; st += 2) {
+        step(st, P0());
+        step(st + 1, P1());
+    }
+    if (st < ns) step(st, P0());
+    // the second K half's partial sums through LDS (over the operand
+    // buffers), added in a fixed order by the first half's waves, which then
+    // apply the gates
+    f4_t *red = reinterpret_cast<f4_t *>(smem) + rg * (16 * 64);
+    if (kh == 1) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) red[((i * 2 + u) * 4 + g) * 64 + lane] = acc[i][u][g];
+    }
+    __syncthreads();
+    if (kh == 0) {
+        const size_t lofs = (size_t)layer * d.H;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                f4_t s[4];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) s[g] = acc[i][u][g] + red[((i * 2 + u) * 4 + g) * 64 + lane];
+                const int uu = 16 * u + (lane & 15), j = j0 + uu;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+                    const int row = 16 * (rg + 4 * i) + 4 * (lane >> 4) + e;
+                    const u64 dp = ptrs[5 * row];
+                    if (dp) {
+                        const float rr = sigmoidf_(s[0][e] + bias[u][0]);
+                        const float z = sigmoidf_(s[1][e] + bias[u][1]);
+                        const float n = tanhf(s[2][e] + bias[u][2] + rr * s[3][e]);
+                        const float hn = (1.0f - z) * n + z * hprev[row * KB_TU + uu];
+                        reinterpret_cast<float *>(dp)[lofs + j] = hn;
+                        const u64 xp = ptrs[5 * row + 4];   // the next layer's bf16 input
+                        if (xp) reinterpret_cast<uint16_t *>(xp)[j] = f32_to_bf16(hn);
+                    }
+                }
+            }
+    }
+    __syncthreads();   // LDS is reused by the next tile
 }
 
 // One launch per layer; the device-side row count picks the path.
@@ -937,9 +1053,9 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
         }
     } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
         gru_medium<BF16W>(d, R, layer, M, smem);
-    } else if (BF16W) {               // 64 x 64 bf16 MFMA tiles through LDS
-        const int ntiles = ((M + G_BM - 1) / G_BM) * (d.H / W_BJ);
-        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) gru_mfma_bf16w(d, R, layer, M, smem, t);
+    } else if (BF16W) {               // 128 x 32-unit bf16 tiles, K split over two wave halves
+        const int ntiles = ((M + KB_BM - 1) / KB_BM) * (d.H / KB_TU);
+        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) gru_kb_bf16(d, R, layer, M, smem, t);
     } else {                          // (16 RB) x 16-unit fp32 tiles, K split over the waves
         const int NR = ks_row_tiles(d, M);
         const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);

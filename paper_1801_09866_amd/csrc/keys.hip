@@ -142,6 +142,12 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
         float v[kSignWords];
 #pragma unroll
         for (int u = 0; u < kSignWords; ++u) v[u] = u < CW ? ldg<float>(x + u * 64 + lane) : 0.0f;
+        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
+            uint16_t *hb = d.f_hbf + (size_t)i * d.LH;
+#pragma unroll
+            for (int u = 0; u < kSignWords; ++u)
+                if (u < CW) hb[u * 64 + lane] = f32_to_bf16(v[u]);
+        }
         words[0] = 0;
 #pragma unroll
         for (int u = 0; u < kSignWords; ++u) {
@@ -158,6 +164,12 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
 #pragma unroll
         for (int s = 0; s < kWordsPerLane / 2; ++s)
             v[s] = lane + 64 * s < CW ? ldg<float4>(x + 4 * (lane + 64 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
+            uint2 *hb = reinterpret_cast<uint2 *>(d.f_hbf + (size_t)i * d.LH);
+#pragma unroll
+            for (int s = 0; s < kWordsPerLane / 2; ++s)
+                if (lane + 64 * s < CW) hb[lane + 64 * s] = pack_bf16x4(v[s]);
+        }
 #pragma unroll
         for (int s = 0; s < kWordsPerLane / 2; ++s) {
             const int w = lane + 64 * s;
@@ -175,6 +187,13 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
 #pragma unroll
         for (int s = 0; s < kWordsPerLane; ++s)
             v[s] = lane + 64 * s < CW ? ldg<float2>(x + 2 * (lane + 64 * s)) : make_float2(0.f, 0.f);
+        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
+            uint32_t *hb = reinterpret_cast<uint32_t *>(d.f_hbf + (size_t)i * d.LH);
+#pragma unroll
+            for (int s = 0; s < kWordsPerLane; ++s)
+                if (lane + 64 * s < CW)
+                    hb[lane + 64 * s] = (uint32_t)f32_to_bf16(v[s].x) | ((uint32_t)f32_to_bf16(v[s].y) << 16);
+        }
 #pragma unroll
         for (int s = 0; s < kWordsPerLane; ++s) {
             const int w = lane + 64 * s;
@@ -272,6 +291,12 @@ __device__ void hist_block_sigdig(const Dev &d, const FrameArgs &f, const Decade
 #pragma unroll
     for (int s = 0; s < kSdWords; ++s)
         v[s] = tid + 256 * s < CW ? ldg<float4>(x + 4 * (tid + 256 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
+    if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
+        uint2 *hb = reinterpret_cast<uint2 *>(d.f_hbf + (size_t)i * d.LH);
+#pragma unroll
+        for (int s = 0; s < kSdWords; ++s)
+            if (tid + 256 * s < CW) hb[tid + 256 * s] = pack_bf16x4(v[s]);
+    }
     u64 words[kSdWords];
     bool bad = false;
     u64 hs = 0;

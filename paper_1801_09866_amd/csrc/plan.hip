@@ -500,6 +500,7 @@ __global__ __launch_bounds__(PT) void k_frame_plan(Dev d0, FrameBlock fb) {
                 d.f_roww[row] = h_w1[r];
                 d.f_rowh[row] = (u64)src;
                 d.f_rowdst[row] = (u64)hp;
+                if (d.wdtype == RNNLM_BF16) d.f_rowhb[row] = (u64)(d.f_hbf + (size_t)i * d.LH);
             }
             if (f.h_status) f.h_status[i] = (uint8_t)st;
             if (f.h_rep) f.h_rep[i] = h_rep[r];
