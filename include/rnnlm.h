@@ -59,13 +59,18 @@ enum { RNNLM_Q_EXACT = 0, RNNLM_Q_SIGN = 1, RNNLM_Q_SIGDIG = 2 };
 /* Weight precision: fp32, or bf16 embedding / GRU / output weights with fp32
  * accumulation (biases and MaxEnt weights stay fp32). */
 enum { RNNLM_F32 = 0, RNNLM_BF16 = 1 };
-/* Per-history status: key cached before this frame (HC_HIT); first of its key
- * in the frame, GRU computed (H_REP); later copy of a key in the frame (H_DUP). */
+/* Per-history status (the history cache of Sec. 3, Fig. 2): key cached before
+ * this frame (HC_HIT); first of its key in the frame, GRU computed (H_REP);
+ * later copy of a key in the frame (H_DUP). */
 enum { RNNLM_H_REP = 0, RNNLM_H_DUP = 1, RNNLM_HC_HIT = 2 };
-/* Per-query status: score computed (COMPUTED); copy of an earlier query of the
- * frame with the same key (Q_DUP); stored score returned (SCORE_HIT). */
+/* Per-query status (the LM-query cache of Sec. 2.4, Fig. 1): score computed
+ * (COMPUTED); copy of an earlier query of the frame with the same key
+ * (Q_DUP); stored score returned (SCORE_HIT). */
 enum { RNNLM_Q_COMPUTED = 0, RNNLM_Q_DUP = 1, RNNLM_Q_SCORE_HIT = 2 };
-/* Sticky device error bits (HANDLE: a null or misaligned history handle). */
+/* Sticky device error bits, for input the method cannot key or score (an id
+ * outside the vocabulary, a value outside the quantiser's domain of Sec. 3,
+ * a query naming no history of its frame; HANDLE: a null or misaligned
+ * history handle). */
 enum { RNNLM_DERR_WORD = 1, RNNLM_DERR_QHIST = 2, RNNLM_DERR_VALUE = 4, RNNLM_DERR_HANDLE = 8 };
 
 typedef struct rnnlm_t rnnlm_t;   /* opaque */
@@ -166,8 +171,11 @@ int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *frame, const rnnlm_out *o
  * failing for any frame enqueues nothing). */
 int rnnlm_score_frames(rnnlm_t *ctx, const rnnlm_frame *frames, const rnnlm_out *outs, int32_t n, void *stream);
 
-/* Empty both caches of every session, zero the statistics and clear the
- * sticky device flag. */
+/* Empty both caches of every session -- the LM-query cache (Sec. 2.4, Fig. 1)
+ * and the history cache (Sec. 3, Fig. 2), for instance between utterances --
+ * zero the statistics and clear the sticky device flag. Asynchronous on
+ * `stream` (fill kernels, no memset); returns RNNLM_EINVAL for a null
+ * context. */
 int rnnlm_cache_reset(rnnlm_t *ctx, void *stream);
 
 /* Full-vocabulary log normaliser (the computation NCE avoids, Sec. 2.2):
@@ -204,15 +212,19 @@ int rnnlm_log_normalizer_static(const float *U_out, const float *b_out, int32_t 
                                 const float *h_top, int32_t n, float *logz, void *stream);
 
 /* Copy the device statistics, summed over all sessions, into *stats (host
- * memory); synchronises `stream`. Returns RNNLM_EDEVICE if the sticky device
- * flag of any session is set (device_error: the OR of all sessions' bits). */
+ * memory); synchronises `stream`. The counts are those Table 1 of Sec. 3
+ * compares across history compressions (unique LM queries = computed, GRU
+ * rows) and the two caches' hits and sizes (Sec. 2.4, Sec. 3). Returns
+ * RNNLM_EDEVICE if the sticky device flag of any session is set
+ * (device_error: the OR of all sessions' bits). */
 int rnnlm_get_stats(rnnlm_t *ctx, rnnlm_stats *stats, void *stream);
 
 /* The same for one session (0 <= session < sessions); a device error in any
  * session still returns RNNLM_EDEVICE. */
 int rnnlm_get_session_stats(rnnlm_t *ctx, int32_t session, rnnlm_stats *stats, void *stream);
 
-/* Test hook: quantise n fp32 elements x with the library's own kernel.
+/* Test hook: quantise n fp32 elements x with the library's own kernel
+ * (the history compression of Sec. 3: sign only, or k significant digits).
  * codes: EXACT -> uint32[n]; SIGDIG -> uint16[n]; SIGN -> uint64[n/64]
  * (n a multiple of 64; element i is bit i%64 of word i/64). err: one device
  * int32 that receives RNNLM_DERR_VALUE if an element was out of domain

@@ -327,15 +327,6 @@ __device__ __forceinline__ void fold_partials(const Dev &d, int n, long long *c,
     __syncthreads();
 }
 
-// 32-bit finaliser of MurmurHash3 (Appleby), for frame-local table placement
-__device__ __forceinline__ uint32_t fmix32(uint32_t h) {
-    h ^= h >> 16;
-    h *= 0x85EBCA6Bu;
-    h ^= h >> 13;
-    h *= 0xC2B2AE35u;
-    return h ^ (h >> 16);
-}
-
 // slot of the order-n MaxEnt n-gram (w-1 .. w-(n-1), target) in a 2^log2 table
 // order-n MaxEnt feature: the order seeds a fold of the n-1 context words
 // (most recent first), then the target; the prefix (everything before the
