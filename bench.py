@@ -9,9 +9,13 @@ MaxEnt scoring, cache admission, h' output). Inputs are resident in HBM
 before timing starts; caches start empty at frame 0 and the first `warmup`
 frames are untimed.
 
-Prints one JSON line (see the keys below). Per-stage kernel times come from a
-replay of the same frames with HIP events around every stage, recorded by the
-library on the stream its kernels run on.
+Prints one JSON line (see the keys below). Per-stage kernel times are the
+mean of three replays of the timed frames (caches reset, the warm-up frames
+run again, so every launch does the same work as in the timed pass), in which
+the library records a HIP event pair around every stage's launches, on the
+stream its kernels run on (rnnlm_profile). The events lengthen the gaps
+between launches (ms_per_step_replay), not the kernels, which is why the
+timed pass runs without them.
 """
 from __future__ import annotations
 
@@ -28,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+REPLAYS = 3   # stamped replays of the timed frames; stage times are their mean
 PEAK = {"hbm_GBs": 8000.0, "fp32_mfma_TFs": 157.3, "bf16_mfma_TFs": 2500.0}
 METRIC = "RNNLM queries/sec (GRU+NCE+MaxEnt), H=1024 V=200k; % of MFMA/HBM roofline"
 
@@ -78,11 +83,12 @@ def qmode_name(qm, k):
     return {0: "exact", 1: "sign", 2: "sigdig%d" % k}[qm]
 
 
-def counter_traffic(workload, stage):
+def counter_traffic(workload, stage, lo, hi):
     """HBM bytes per launch of `stage` (FETCH_SIZE + WRITE_SIZE, scaled by the
-    plain-copy calibration) from the committed counter summaries under
-    profiles/, or None when none covers this workload or the kernel's sources
-    have changed since the counters were taken."""
+    plain-copy calibration) over frames lo..hi of the first leg, from the
+    committed counter summaries under profiles/, or None when none covers this
+    workload and frame span or the kernel's sources have changed since the
+    counters were taken."""
     import glob
 
     from paper_1801_09866_amd.profsum import KERNELS, source_sha
@@ -90,11 +96,12 @@ def counter_traffic(workload, stage):
     if files is None:
         return None
     sha = source_sha(files)
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_counters_*.txt"))):
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
         with open(path) as fh:
             for line in fh:
                 parts = line.split()
-                if len(parts) == 6 and parts[0] == "traffic" and parts[1] == workload and parts[2] == stage:
+                if len(parts) == 6 and parts[0] == "traffic" and parts[2] == stage \
+                        and parts[1] == "%s:frames%d-%d" % (workload, lo, hi):
                     kv = dict(x.split("=", 1) for x in parts[3:])
                     if kv.get("source_sha256") == sha:
                         return int(kv["fetch_bytes"]) + int(kv["write_bytes"])
@@ -229,15 +236,22 @@ def main():
     log("timed %d frames: %.3f ms GPU (%.3f ms wall), %.0f queries/s" % (K, gpu_ms, wall * 1e3, value))
 
     # ---- per-stage kernel times: replay the same frames with events ------
-    stages, roofline = {}, None
+    stages, roofline, stamped_ms = {}, None, None
     if not args.no_replay:
-        sc.reset()
-        run(0, W)
-        sc.profile(R.STAGES[:4])
-        run(W, n_frames)
-        torch.cuda.synchronize()
-        prof = sc.profile_read()
-        sc.profile(())
+        prof, stamped_ms = {}, 0.0
+        for _ in range(REPLAYS):
+            sc.reset()
+            run(0, W)
+            sc.profile(R.STAGES[:4])
+            torch.cuda.synchronize()
+            ev0.record(stream)
+            run(W, n_frames)
+            ev1.record(stream)
+            torch.cuda.synchronize()
+            stamped_ms += ev0.elapsed_time(ev1) / REPLAYS
+            for name, (ms, launches) in sc.profile_read().items():
+                prof[name] = (prof.get(name, (0.0, 0))[0] + ms / REPLAYS, launches)
+            sc.profile(())
         work = algorithmic_work(cfg, span, qm, K)
         for name, (ms, launches) in prof.items():
             entry = {"ms_total": round(ms, 4), "launches": launches, "us_per_launch": round(1e3 * ms / launches, 2)}
@@ -257,9 +271,13 @@ def main():
         e = stages[dom]
         roofline = {"kernel": dom, "bound": e["bound"], "achieved": e["achieved"], "peak": e["peak"],
                     "unit": e["unit"], "frac": e["frac"],
-                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), dom),
+                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), dom, W, n_frames - 1),
                     "algorithmic_per_launch": round(e["algorithmic"] / e["launches"]),
                     "us_per_launch": e["us_per_launch"]}
+        if dom == "gru_gemm":
+            roofline["gru_rows_per_launch"] = round(span["gru_rows"] / K, 2)
+        rows = rows_by_frame(sc, run, W, n_frames)
+        log("gru rows by frame %d..%d: %s" % (W, n_frames - 1, rows))
         log("stages:", json.dumps(stages))
 
     # ---- per-frame latency, and the rate with each frame's block over PCIe --
@@ -289,6 +307,7 @@ def main():
         "steps": K, "warmup": W, "ms_per_step": round(gpu_ms / K, 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16-weights/f32-accumulate" if m.wdtype == 1 else "f32", "data": "synthetic",
+        "ms_per_step_replay": round(stamped_ms / K, 5) if stamped_ms else None,
         "config": {"workload": "%s_%s: V=%d E=%d H=%d L=%d MaxEnt 2^%d orders 2..%d, %d queries/frame"
                                % (cfg.name, qmode_name(qm, qk), m.V, m.E, m.H, m.L, m.maxent_log2,
                                   m.maxent_order, cfg.queries),
@@ -300,11 +319,29 @@ def main():
         "hist_hit_ratio": hit(span["hist_hits"], span["hists"]),
         "wall_ms": round(wall * 1e3, 3),
         "roofline": roofline,
+        "gru_rows_by_frame": rows if roofline else None,
         "stages": stages,
         "frame_io": io,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def rows_by_frame(sc, run, W, n):
+    """GRU rows of each of frames W..n-1 (one frame at a time, the statistics
+    read after each), at most 200 frames."""
+    import torch
+    sc.reset()
+    run(0, W)
+    torch.cuda.synchronize()
+    prev = sc.stats()["gru_rows"]
+    out = []
+    for i in range(W, min(n, W + 200)):
+        run(i, i + 1)
+        cur = sc.stats()["gru_rows"]
+        out.append(cur - prev)
+        prev = cur
+    return out
 
 
 def hip_runtime():
@@ -450,23 +487,31 @@ def cpu_baseline(args, wl, qm, qk, sc, run, frames):
     cfg, m = wl.cfg, wl.cfg.model
 
     def sample(budget):
-        o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
-                   cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
+        """Whole frames from frame 0 and empty caches until the budget is
+        spent; when every frame is done first, the pass starts again from a
+        new oracle (empty caches). Returns (frames of the longest pass, passes
+        begun, queries, seconds)."""
         t = time.perf_counter()
-        nq = S = 0
-        for fr in wl.frames:
-            o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
-            nq += fr.n_query
-            S += 1
-            if time.perf_counter() - t >= budget:
-                break
-        return S, nq, time.perf_counter() - t
+        nq = S = passes = 0
+        while time.perf_counter() - t < budget:
+            o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, wl.weights, qm, qk,
+                       cap_hist=cfg.cap_hist, cap_query=cfg.cap_query)
+            passes += 1
+            for i, fr in enumerate(wl.frames):
+                o.score_frame(wl.pool.vec[fr.pool_idx], fr.hist_words, fr.q_hist, fr.q_tgt)
+                nq += fr.n_query
+                S = max(S, i + 1)
+                if time.perf_counter() - t >= budget:
+                    break
+        return S, passes, nq, time.perf_counter() - t
 
-    S, nq, secs = sample(args.cpu_seconds)
+    S, passes, nq, secs = sample(args.cpu_seconds)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    with threadpool_limits(limits=1):   # the same oracle on one thread, over a shorter prefix
-        S1, nq1, secs1 = sample(args.cpu_seconds / 3)
-    # the GPU on exactly the same frames (cold caches, frame 0 on)
+    with threadpool_limits(limits=1):   # the same oracle on one thread, over a shorter budget
+        S1, passes1, nq1, secs1 = sample(args.cpu_seconds / 3)
+    what = lambda S, p: "frames 0..%d" % (S - 1) + (" x %d passes" % p if p > 1 else "")
+    frames_q = wl.frames
+    # the GPU on the same frames (cold caches, frame 0 on)
     sc.reset()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -475,13 +520,13 @@ def cpu_baseline(args, wl, qm, qk, sc, run, frames):
     e1.record()
     torch.cuda.synchronize()
     gsec = e0.elapsed_time(e1) / 1e3
-    log("oracle: %d frames, %d queries in %.1fs" % (S, nq, secs))
+    log("oracle: %s, %d queries in %.1fs" % (what(S, passes), nq, secs))
     return {"value": round(nq / secs, 1), "unit": "queries/s", "cores": int(threads), "kind": "oracle",
-            "sample": "frames 0..%d of the same workload from empty caches (%d queries, %.1f s)"
-                      % (S - 1, nq, secs),
-            "gpu_value_same_sample": round(nq / gsec, 1),
+            "sample": "%s of the same workload from empty caches (%d queries, %.1f s)"
+                      % (what(S, passes), nq, secs),
+            "gpu_value_same_frames": round(sum(f.n_query for f in frames_q[:S]) / gsec, 1),
             "value_1_thread": round(nq1 / secs1, 1),
-            "sample_1_thread": "frames 0..%d (%d queries, %.1f s)" % (S1 - 1, nq1, secs1)}
+            "sample_1_thread": "%s (%d queries, %.1f s)" % (what(S1, passes1), nq1, secs1)}
 
 
 METRIC_CHECK = "full-vocabulary log-normalisers/sec (GRU step + logsumexp over V), H=1024 V=200k; % of fp32 MFMA roofline"
@@ -581,7 +626,8 @@ def main_check(args, cfg):
         g = stages["lognorm_gemm"]
         roofline = {"kernel": "lognorm_gemm", "bound": "mfma", "achieved": g["achieved"], "peak": g["peak"],
                     "unit": "TFLOP/s", "frac": g["frac"],
-                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), "lognorm_gemm"),
+                    "traffic": counter_traffic("%s_%s" % (cfg.name, qmode_name(qm, qk)), "lognorm_gemm",
+                                               W, n_frames - 1),
                     "us_per_launch": g["us_per_launch"]}
         log("stages:", json.dumps(stages))
 

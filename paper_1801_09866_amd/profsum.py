@@ -22,6 +22,18 @@ tell whether the kernel has changed since the counters were taken.
 
 The third form summarises bench.py --sweep: per library kernel and sweep
 size, mean duration, HBM bytes and MFMA utilisation per launch.
+
+    python -m paper_1801_09866_amd.profsum --span WORKLOAD --warmup W --steps K \
+        --trace DIR [--fetch DIR --write DIR --fetch-scale B --write-scale B] [--mfma DIR] [--leg 0[,1..]]
+
+The fourth form selects the frames bench.py times: a frame is the run of
+library kernels that starts with one k_hist_key launch, a leg is the run of
+frames after one cache reset (the fill launches of rnnlm_cache_reset), and
+the timed frames are frames W .. W+K-1 of leg 0 (the first leg; legs 1..3 are
+bench.py's stamped replays of the same frames). It prints, per library kernel, the launches and
+mean duration over those frames from the kernel trace, the mean HBM bytes and
+MFMA counters from the counter runs, one line per frame for the GRU, and
+traffic lines for WORKLOAD:framesW-E as in the second form.
 """
 import argparse
 import collections
@@ -166,6 +178,102 @@ def traffic(a):
               % (a.traffic, st[0], fb, wb, source_sha(st[1])))
 
 
+def dispatch_rows(d, trace=False):
+    """[(dispatch id, kernel, {name: value})] in dispatch order: from a kernel
+    trace (name "ns": the duration) or from a counter run."""
+    if trace:
+        return [(i, k, {"ns": float(ns)}) for i, k, ns in trace_dispatches(d)]
+    rows = collections.defaultdict(dict)
+    kern = {}
+    for p in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(p) as f:
+            for r in csv.DictReader(f):
+                i = int(r["Dispatch_Id"])
+                rows[i][r["Counter_Name"]] = rows[i].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                kern[i] = r["Kernel_Name"]
+    return [(i, kern[i], rows[i]) for i in sorted(rows)]
+
+
+def by_frame(rows, leg):
+    """Split dispatch rows into the frames of leg `leg`: [[(kernel family, values)]]."""
+    frames, cur_leg, seen = [], 0, False
+    for _, k, v in rows:
+        fam = family(k)
+        if fam == "rn::k_fill_u32":
+            if seen:                 # a cache reset after frames: the next leg
+                cur_leg += 1
+                seen = False
+            continue
+        if fam == "rn::k_hist_key":
+            seen = True
+        if cur_leg != leg or stage_of(k) is None:
+            continue
+        if fam == "rn::k_hist_key":
+            frames.append([])
+        if frames:
+            frames[-1].append((fam, v))
+    return frames
+
+
+def span(a):
+    lo, hi = a.warmup, a.warmup + a.steps
+    legs = [int(x) for x in str(a.leg).split(",")]
+
+    def select(d, trace=False):
+        rows = dispatch_rows(d, trace)
+        out = []
+        for g in legs:
+            fr = by_frame(rows, g)
+            if len(fr) < hi:
+                raise SystemExit("leg %d of %s holds %d frames, fewer than %d" % (g, d, len(fr), hi))
+            out.append(fr[lo:hi])
+        return out          # [leg][frame] -> [(kernel family, values)]
+
+    runs = {"ns": select(a.trace, trace=True)}
+    for key, d in (("fetch", a.fetch), ("write", a.write), ("mfma", a.mfma)):
+        if d:
+            runs[key] = select(d)
+    scale = {"FETCH_SIZE": a.fetch_scale or 0.0, "WRITE_SIZE": a.write_scale or 0.0}
+    per = collections.defaultdict(lambda: collections.defaultdict(list))
+    for key, by_leg in runs.items():
+        for fr in by_leg:
+            for f in fr:
+                for fam, v in f:
+                    for c, x in v.items():
+                        per[fam][c].append(x * scale.get(c, 1.0))
+    mean = lambda v: sum(v) / len(v) if v else float("nan")
+    print("# frames %d..%d of leg %s (%d frames%s)" % (lo, hi - 1, a.leg, hi - lo,
+                                                     ", means over the legs" if len(legs) > 1 else ""))
+    cols = sorted({c for v in per.values() for c in v if c != "ns"})
+    print("%-24s %8s %10s " % ("kernel", "launches", "avg_us") + " ".join("%16s" % c for c in cols))
+    for fam in sorted(per, key=lambda f: -sum(per[f]["ns"])):
+        print("%-24s %8d %10.2f " % (fam, len(per[fam]["ns"]), mean(per[fam]["ns"]) / 1e3)
+              + " ".join("%16.1f" % mean(per[fam][c]) if per[fam].get(c) else "%16s" % "-" for c in cols))
+    print("# per frame, rn::k_gru (bytes: counter units times the calibration scales)")
+    print("%6s %10s %14s %14s %10s %12s %12s" % ("frame", "us", "MfmaFlopsF32", "MfmaFlopsBF16", "MfmaUtil",
+                                                  "fetch_MB", "write_MB"))
+    for i in range(lo, hi):
+        def val(key, c):
+            if key not in runs:
+                return float("nan")
+            per_leg = []
+            for fr in runs[key]:
+                xs = [v.get(c, 0.0) for fam, v in fr[i - lo] if fam == "rn::k_gru"]
+                per_leg.append(sum(xs) if c != "MfmaUtil" else mean(xs))
+            return mean(per_leg)
+        print("%6d %10.2f %14.0f %14.0f %10.1f %12.2f %12.2f" % (
+            i, val("ns", "ns") / 1e3, val("mfma", "MfmaFlopsF32"), val("mfma", "MfmaFlopsBF16"),
+            val("mfma", "MfmaUtil"), val("fetch", "FETCH_SIZE") * scale["FETCH_SIZE"] / 1e6,
+            val("write", "WRITE_SIZE") * scale["WRITE_SIZE"] / 1e6))
+    if a.fetch and a.write:
+        for fam in sorted(per):
+            st = KERNELS.get(fam)
+            if st and per[fam].get("FETCH_SIZE") and per[fam].get("WRITE_SIZE"):
+                print("traffic %s:frames%d-%d %s fetch_bytes=%d write_bytes=%d source_sha256=%s"
+                      % (a.span, lo, hi - 1, st[0], mean(per[fam]["FETCH_SIZE"]), mean(per[fam]["WRITE_SIZE"]),
+                         source_sha(st[1])))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("dir", nargs="?")
@@ -179,7 +287,14 @@ def main():
     ap.add_argument("--sweep-trace", default=None, help="saturation sweep: the kernel-trace run's directory")
     ap.add_argument("--mfma", default=None, help="saturation sweep: an MfmaUtil counter run's directory")
     ap.add_argument("--group", type=int, default=6, help="saturation sweep: launches per size")
+    ap.add_argument("--span", default=None, help="bench frames: the workload name for traffic lines")
+    ap.add_argument("--trace", default=None, help="bench frames: the kernel-trace run's directory")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--leg", default="0", help="leg index, or several joined by commas")
     a = ap.parse_args()
+    if a.span:
+        return span(a)
     if a.sweep_trace:
         return sweep(a)
     if a.traffic:
