@@ -20,24 +20,10 @@ namespace rn {
 typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8_t __attribute__((ext_vector_type(8)));
 
-constexpr int G_BM = 64;    // work-list rows per block
 constexpr int G_THREADS = 512;
 
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 
-// block -> (row tile, unit tile); blocks are dealt to the 8 XCDs round-robin,
-// so give every XCD its own set of unit tiles: each XCD then streams only
-// 1/8 of the weights, which stay resident in its L2.
-__device__ __forceinline__ void gru_tile_of(int b, int NJ, int &mt, int &jt) {
-    if ((NJ & 7) == 0) {
-        const int xcd = b & 7, idx = b >> 3, per = NJ >> 3;
-        mt = idx / per;
-        jt = xcd + 8 * (idx % per);
-    } else {
-        mt = b / NJ;
-        jt = b % NJ;
-    }
-}
 
 struct RowSrc {
     const void *x;      // start of this row's x part (fp32, or bf16 embedding)
@@ -172,137 +158,6 @@ __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
 // One LDS buffer serves every path.
 constexpr int G_LDS_FLOATS = 35840;   // 140 KB
 
-// ------------------------ medium path (32 < rows <= 256) -------------------
-// Tiles of 16 rows x 16 hidden units; the block's 8 waves split K, each
-// accumulating the four gate tiles (reset, update, candidate input part,
-// candidate recurrent part) of its K range with MFMAs fed straight from
-// global memory (16 B per lane per operand and step), md_ch steps in flight
-// at once, double-buffered; then the partial tiles are summed through LDS and
-// wave 0 applies the gates.
-constexpr int MD_MAXROWS = 256;
-// steps per chunk: bf16 packs its A operand from two fp32 loads, so it keeps
-// one step per chunk to stay within the register file
-template <bool BF16W>
-constexpr int md_ch() { return BF16W ? 1 : 2; }
-
-template <bool BF16W>
-struct MdOps {
-    using T = typename std::conditional<BF16W, uint4, float4>::type;
-    T a[md_ch<BF16W>()], r[md_ch<BF16W>()], z[md_ch<BF16W>()], n[md_ch<BF16W>()];
-};
-
-// one K step of one gate tile: fp32 takes 4 k per lane (four 16x16x4 MFMAs
-// over the float4's components), bf16 takes 8 (one 16x16x32 MFMA)
-__device__ __forceinline__ f4_t md_mfma(float4 a, float4 b, f4_t c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
-}
-__device__ __forceinline__ f4_t md_mfma(uint4 a, uint4 b, f4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8_t, a), __builtin_bit_cast(bf8_t, b), c, 0, 0, 0);
-}
-
-template <bool BF16W>
-__device__ __forceinline__ void gru_medium(const Dev &d, const Rows &R, int layer, int M, float *smem) {
-    using T = typename MdOps<BF16W>::T;
-    using E = typename std::conditional<BF16W, uint16_t, float>::type;
-    constexpr int CH = md_ch<BF16W>();
-    const int NJ = d.H / 16;
-    const int ntiles = ((M + 15) / 16) * NJ;
-    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
-    const int Kx = layer == 0 ? d.E : d.H, K = Kx + d.H;
-    constexpr int KS = BF16W ? 32 : 16;            // k per step
-    const int nsteps = K / KS;
-    const int s0 = (w * nsteps) / 8, s1 = ((w + 1) * nsteps) / 8;   // scalars
-    const int row = lane & 15, kq = (KS / 4) * (lane >> 4);
-    const E *Wp = reinterpret_cast<const E *>(d.Wl);
-    for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-        int mt, jt;
-        if ((NJ & 7) == 0) {   // every XCD keeps its own unit tiles (and weights)
-            const int xcd = tile & 7, idx = tile >> 3, per = NJ >> 3;
-            mt = idx / per;
-            jt = xcd + 8 * (idx % per);
-        } else {
-            mt = tile / NJ;
-            jt = tile % NJ;
-        }
-        const int m0 = mt * 16, j0 = jt * 16;
-        const RowSrc src = row_source(d, R, layer, m0 + row, M);
-        const E *pr = Wp + (size_t)(j0 + row) * K + kq, *pz = Wp + (size_t)(d.H + j0 + row) * K + kq,
-                *pn = Wp + (size_t)(2 * d.H + j0 + row) * K + kq;
-        auto loadA = [&](int k) -> T {
-            if (!src.valid) return T{0, 0, 0, 0};
-            if (!BF16W) {
-                const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
-                return __builtin_bit_cast(T, ldg<float4>(p));
-            }
-            if (k < Kx && src.x_bf16)
-                return __builtin_bit_cast(T, ldg<uint4>(reinterpret_cast<const uint16_t *>(src.x) + k));
-            const float *p = k < Kx ? reinterpret_cast<const float *>(src.x) + k : src.h + (k - Kx);
-            return __builtin_bit_cast(T, pack_bf16x8(ldg<float4>(p), ldg<float4>(p + 4)));
-        };
-        auto load = [&](MdOps<BF16W> &o, int sc) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int st = sc + c;
-                if (st < s1) {
-                    const int k = st * KS;
-                    o.a[c] = loadA(k + kq);
-                    o.r[c] = ldg<T>(pr + k);
-                    o.z[c] = ldg<T>(pz + k);
-                    o.n[c] = ldg<T>(pn + k);
-                }
-            }
-        };
-        f4_t ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-        auto compute = [&](const MdOps<BF16W> &o, int sc) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int st = sc + c;
-                if (st < s1) {
-                    ar = md_mfma(o.a[c], o.r[c], ar);
-                    az = md_mfma(o.a[c], o.z[c], az);
-                    if (st * KS < Kx) anx = md_mfma(o.a[c], o.n[c], anx);
-                    else anh = md_mfma(o.a[c], o.n[c], anh);
-                }
-            }
-        };
-        MdOps<BF16W> b0, b1;
-        load(b0, s0);
-        for (int sc = s0; sc < s1; sc += 2 * CH) {
-            load(b1, sc + CH);
-            compute(b0, sc);
-            load(b0, sc + 2 * CH);
-            compute(b1, sc + CH);
-        }
-        // sum the waves' partial tiles, then the gates (wave 0)
-        float *red = smem + (size_t)(w * 64 + lane) * 16;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            red[e] = ar[e];
-            red[4 + e] = az[e];
-            red[8 + e] = anx[e];
-            red[12 + e] = anh[e];
-        }
-        __syncthreads();
-        if (w == 0) {
-            for (int v = 1; v < 8; ++v) {
-                const float *o = smem + (size_t)(v * 64 + lane) * 16;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    ar[e] += o[e];
-                    az[e] += o[4 + e];
-                    anx[e] += o[8 + e];
-                    anh[e] += o[12 + e];
-                }
-            }
-            gru_epilogue(d, R, layer, M, m0, j0, 0, 0, ar, az, anx, anh);
-        }
-        __syncthreads();   // the partial tiles are reused by the next tile
-    }
-}
-
 // ------------------------ narrow path (few rows) ---------------------------
 // A frame with few new keys is bound by reading the weights once and by
 // memory latency, not by FLOPs. Every block owns 4 hidden units for all rows,
@@ -318,6 +173,19 @@ constexpr int N_MAXROWS = 32;   // rows handled by the narrow path at most
 constexpr int N_TILES = N_MAXROWS / 16;
 template <bool BF16W>
 constexpr int n_pass() { return BF16W ? 8 : 12; }   // steps whose operands are loaded together
+
+// One K step of one gate tile from 16 bytes of operands per lane: fp32
+// takes 4 k per lane (four 16x16x4 MFMAs over the float4's components), bf16
+// takes 8 (one 16x16x32 MFMA).
+__device__ __forceinline__ f4_t nw_mfma(float4 a, float4 b, f4_t c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+}
+__device__ __forceinline__ f4_t nw_mfma(uint4 a, uint4 b, f4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8_t, a), __builtin_bit_cast(bf8_t, b), c, 0, 0, 0);
+}
 
 // Operands of the narrow path that do not depend on the frame's row count.
 // The kernel issues these loads as it starts, so that they are in flight
@@ -363,7 +231,7 @@ __device__ __forceinline__ void narrow_preload(const Dev &d, const SessList &sl,
 template <bool BF16W, bool USE_PRE, int NT>
 __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int layer, int M, float *smem, int g,
                                            const NarrowPre<BF16W> &pre) {
-    using T = typename MdOps<BF16W>::T;
+    using T = typename std::conditional<BF16W, uint4, float4>::type;
     using E = typename std::conditional<BF16W, uint16_t, float>::type;
     constexpr int KS = BF16W ? 32 : 16;   // k per step
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
@@ -465,8 +333,8 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
                     if (t < nt) {
-                        if (xp) accx[t] = md_mfma(a[t][c], b[c], accx[t]);
-                        else acch[t] = md_mfma(a[t][c], b[c], acch[t]);
+                        if (xp) accx[t] = nw_mfma(a[t][c], b[c], accx[t]);
+                        else acch[t] = nw_mfma(a[t][c], b[c], acch[t]);
                     }
                 }
             }
@@ -504,7 +372,7 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
     }
 }
 
-// ------------------------------- fp32 -------------------------------------
+// -------------------- tiled path (more than 32 rows): fp32 ------------------
 // Tiles of BM = 16 * RB rows x 16 hidden units (48 weight rows: the units'
 // reset, update and candidate rows). The row-tile height follows the row
 // count: R row tiles per unit tile, with R chosen so that R x (H / 16) tiles
@@ -605,6 +473,55 @@ struct KsEpi {
     size_t lofs;         // this layer's offset in a destination row
 };
 
+// The end of a tile, for a wave of row group G holding NRB row blocks' four
+// accumulators per gate part. Rounds of two row blocks (2p from group 0,
+// 2p + 1 from group 1): the waves write their partial sums, [area p & 1]
+// [group][K quarter][part][lane], over the operand buffers; thread (h, i, u)
+// then sums the four K quarters of row i, unit u of row block 2p + h in a
+// fixed order and applies the gates. NP: u64 pointers per tile row (the
+// destination first; with 5, the fifth is where the bf16 copy of h' goes for
+// the next layer, or 0).
+template <int RB, int G, int NP>
+__device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], float *smem,
+                                         const KsEpi &ep, int w, int lane, int tid) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    const float *red = smem;
+    const int h = tid >> 8, ei = (tid >> 4) & 15, eu = tid & 15;
+#pragma unroll
+    for (int p = 0; p < (RB + 1) / 2; ++p) {
+        if (p < NRB) {
+            float4 *r = reinterpret_cast<float4 *>(smem) + (((p & 1) * 2 + G) * 4 + (w & 3)) * (4 * 64);
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                r[g * 64 + lane] = make_float4(acc[p][g][0], acc[p][g][1], acc[p][g][2], acc[p][g][3]);
+        }
+        __syncthreads();
+        const int rb = 2 * p + h;
+        if (rb < RB) {   // wave-uniform
+            // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+            const float *rf = red + ((p & 1) * 2 + h) * (4 * 4 * 256) + (16 * (ei >> 2) + eu) * 4 + (ei & 3);
+            float sg[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) sg[g] += rf[(q * 4 + g) * 256];
+            const int row = 16 * rb + ei;
+            const u64 dp = ep.ptrs[NP * row];
+            if (dp) {
+                const float rr = sigmoidf_(sg[0] + ep.br);
+                const float z = sigmoidf_(sg[1] + ep.bz);
+                const float n = tanhf(sg[2] + ep.bn + rr * sg[3]);
+                const float hn = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
+                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+                if constexpr (NP == 5) {
+                    const u64 xp = ep.ptrs[NP * row + 4];
+                    if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
+                }
+            }
+        }
+    }
+}
+
 // The K loop, the partial sums and the gates, as run by a wave of row group
 // G (wave-uniform). Every wave runs the same barriers whatever its group.
 template <int RB, int G>
@@ -656,41 +573,7 @@ __device__ __forceinline__ void ks_waves(KsLds As, float *smem, const KsEpi &ep,
         step(kt + 1, Hh(), P1());
     }
     if (kt < nk) step(kt, Hh(), P0());
-    // Rounds of two row blocks (2p from group 0, 2p + 1 from group 1): the
-    // waves write their partial sums, [area p & 1][group][K quarter][part]
-    // [lane], over the operand buffers; thread (h, i, u) then sums the four K
-    // quarters of row i, unit u of row block 2p + h in a fixed order and
-    // applies the gates.
-    const float *red = smem;
-    const int h = tid >> 8, ei = (tid >> 4) & 15, eu = tid & 15;
-#pragma unroll
-    for (int p = 0; p < (RB + 1) / 2; ++p) {
-        if (p < NRB) {
-            float4 *r = reinterpret_cast<float4 *>(smem) + (((p & 1) * 2 + G) * 4 + (w & 3)) * (4 * 64);
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                r[g * 64 + lane] = make_float4(acc[p][g][0], acc[p][g][1], acc[p][g][2], acc[p][g][3]);
-        }
-        __syncthreads();
-        const int rb = 2 * p + h;
-        if (rb < RB) {   // wave-uniform
-            // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
-            const float *rf = red + ((p & 1) * 2 + h) * (4 * 4 * 256) + (16 * (ei >> 2) + eu) * 4 + (ei & 3);
-            float sg[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) sg[g] += rf[(q * 4 + g) * 256];
-            const int row = 16 * rb + ei;
-            const u64 dp = ep.ptrs[3 * row];
-            if (dp) {
-                const float rr = sigmoidf_(sg[0] + ep.br);
-                const float z = sigmoidf_(sg[1] + ep.bz);
-                const float n = tanhf(sg[2] + ep.bn + rr * sg[3]);
-                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
-            }
-        }
-    }
+    ks_gates<RB, G, 3>(acc, smem, ep, w, lane, tid);
 }
 
 template <int RB>
@@ -768,26 +651,25 @@ __device__ __forceinline__ void gru_ks_f32(const Dev &d, const Rows &R, int laye
     __syncthreads();   // LDS is reused by the next tile
 }
 
-// ------------------------------- bf16 -------------------------------------
-// Tiles of 128 rows x 32 hidden units (96 weight rows), K in steps of 128
-// through double-buffered LDS, all operands bf16: the history rows were
-// rounded once per frame by the keys kernel, and the second layer's input is
-// the bf16 copy of the first layer's h' that its tiles' epilogue writes, so a
-// tile moves 2 bytes per operand element and converts nothing. The 8 waves
-// are 4 row groups x 2 K halves: wave w takes the row blocks g and g + 4
-// (g = w % 4) and k = 64 (w / 4) .. + 63 of every step, 32 k per
-// 16 x 16 x 32 MFMA; waves w and w + 4 share a SIMD and the same rows. The two
-// K halves' partial sums meet in LDS (in a fixed order) and the first half's
-// waves apply the gates.
-constexpr int KB_BM = 128, KB_TU = 32, KB_BK = 128, KB_LDA = KB_BK + 8;   // LDA in bf16
-constexpr int KB_ROWS = KB_BM + 3 * KB_TU;                                // A rows, then the weight rows
-constexpr int KB_OPER = 2 * KB_ROWS * KB_LDA / 2;                         // two operand buffers (floats)
-constexpr int KB_PTRS = KB_OPER;                                          // [128][5] u64 per tile row
-constexpr int KB_HPREV = KB_PTRS + KB_BM * 10;                            // [128][32] fp32 h
-static_assert(KB_HPREV + KB_BM * KB_TU <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
-static_assert(4 * 16 * 64 * 4 <= KB_OPER, "bf16 partial sums exceed the operand buffers");
+// -------------------- tiled path (more than 32 rows): bf16 ------------------
+// The fp32 tile's shape and schedule (16 RB rows x 16 hidden units, 8 waves as
+// 2 row groups x 4 K quarters, double-buffered LDS, loads three steps ahead)
+// with bf16 operands: the history rows were rounded once per frame by the
+// keys kernel, and the second layer's input is the bf16 copy of the first
+// layer's h' that its tiles' epilogue writes. A step is 128 k, i.e. the same
+// 256 bytes per operand row as an fp32 step, so the LDS layout and every LDS
+// address are the fp32 tile's; a wave's quarter is 32 k, one 16 x 16 x 32 MFMA
+// per row block and gate part. A step may straddle the input / history
+// boundary or reach past K (E and H are multiples of 64): each 8-k chunk is
+// loaded from its own part (clamped inside K), and a wave's quarter, which
+// lies wholly in one part (or past K), feeds zeros to the candidate gate's
+// other accumulator (or to every product).
+constexpr int KSB_BK = 128;                               // K step (bf16 elements)
+constexpr int KSB_PTRS = KS_OPER;                         // per tile row: dst, h fp32, h bf16, x bf16, x copy dst
+constexpr int KSB_HPREV = KSB_PTRS + 16 * KS_RBMAX * 10;  // per tile row: h of the tile's 16 units
+static_assert(KSB_HPREV + 16 * KS_RBMAX * KS_TU <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
 
-// address of element `idx` of row m of a per-session per-row array of `stride` elements
+// start of row m of a per-session per-row array of `stride` elements
 template <class T>
 __device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t stride) {
     long long o = R.sofs[0];
@@ -803,71 +685,143 @@ __device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t strid
     return shift_ptr(arr, o) + (size_t)(m - base) * stride;
 }
 
-// The register stage of one K step: 4 A chunks and 3 weight chunks of 8
-// bf16 per thread (thread t: rows t/16 + 32 j, chunk t % 16).
-struct KbStage {
-    uint4 v[7];
+template <int NPA>
+struct KsbStage {
+    uint4 a[NPA], b0, b1;
 };
 
-// One K step of a wave: per 32-k depth, its two row blocks x two unit blocks
-// x (reset, update, candidate input part, candidate history part). The
-// candidate gate's weight fragment feeds both of its accumulators, with zeros
-// in place of the part the depth does not lie in (and every fragment zero for
-// a depth past K), so that one branch-free instruction stream serves every
-// step; the extra MFMAs are cheap next to the bytes a bf16 step moves.
-__device__ __forceinline__ void kb_mfma(f4_t (&acc)[2][2][4], const uint16_t (*As)[KB_LDA], int rg, int kh, int lane,
-                                        int k0, int Kx, int K) {
-    const int fr = lane & 15, fk = 8 * (lane >> 4);
+// Every thread issues the same loads, none behind a branch: a chunk past K
+// re-reads the last chunk inside K (its products are zeroed), rows past the
+// tile re-read its last row. bp0, bp1: the starts of the thread's weight rows.
+template <int RB>
+__device__ __forceinline__ void ksb_load(KsbStage<(16 * RB + 31) / 32> &S, const u64 *ptrs, int a_r, int a_k, int k0,
+                                         int Kx, int K, const uint16_t *bp0, const uint16_t *bp1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+    const int k = min(k0 + a_k, K - 8);
+    const bool xp = k < Kx;
 #pragma unroll
-    for (int kd = 0; kd < 2; ++kd) {
-        const int kr = 64 * kh + 32 * kd;   // wave-uniform
-        const bool live = k0 + kr < K, xp = k0 + kr < Kx;
-        const uint4 z = make_uint4(0, 0, 0, 0);
-        bf8_t a[2], b[2][4];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const uint4 v = *reinterpret_cast<const uint4 *>(&As[16 * (rg + 4 * i) + fr][kr + fk]);
-            a[i] = __builtin_bit_cast(bf8_t, live ? v : z);
-        }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            uint4 g[3];
-#pragma unroll
-            for (int q = 0; q < 3; ++q)
-                g[q] = *reinterpret_cast<const uint4 *>(&As[KB_BM + q * KB_TU + 16 * u + fr][kr + fk]);
-            b[u][0] = __builtin_bit_cast(bf8_t, g[0]);
-            b[u][1] = __builtin_bit_cast(bf8_t, g[1]);
-            b[u][2] = __builtin_bit_cast(bf8_t, xp ? g[2] : z);
-            b[u][3] = __builtin_bit_cast(bf8_t, xp ? z : g[2]);
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    acc[i][u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[u][q], acc[i][u][q], 0, 0, 0);
+    for (int p = 0; p < NPA; ++p) {
+        const int row = min(a_r + 32 * p, BM - 1);
+        const uint16_t *src = reinterpret_cast<const uint16_t *>(ptrs[5 * row + (xp ? 3 : 2)]);
+        S.a[p] = ldg<uint4>(src + (xp ? k : k - Kx));
     }
+    S.b0 = ldg<uint4>(bp0 + k);
+    S.b1 = ldg<uint4>(bp1 + k);
 }
 
-__device__ __forceinline__ void gru_kb_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile) {
-    const int NU = d.H / KB_TU;
-    int mt, jt;
-    gru_tile_of(tile, NU, mt, jt);
-    const int m0 = mt * KB_BM, j0 = jt * KB_TU;
-    if (m0 >= M) return;   // block-uniform
+template <int RB>
+__device__ __forceinline__ void ksb_store(const KsbStage<(16 * RB + 31) / 32> &S, KsLds As, int buf, int a_r, int a_c,
+                                          bool has_b1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (a_r + 32 * p < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r + 32 * p][a_c]) = S.a[p];
+    *reinterpret_cast<uint4 *>(&As[buf][BM + a_r][a_c]) = S.b0;
+    if (has_b1) *reinterpret_cast<uint4 *>(&As[buf][BM + 32 + a_r][a_c]) = S.b1;
+}
 
-    auto As = reinterpret_cast<uint16_t (*)[KB_ROWS][KB_LDA]>(smem);
-    u64 *ptrs = reinterpret_cast<u64 *>(smem + KB_PTRS);   // per row: dst, h fp32, h bf16, x bf16, x copy dst
-    float *hprev = smem + KB_HPREV;
+// One K step of a wave of row group G: its row blocks G, G + 2, ... x
+// (reset, update, candidate input part, candidate history part) over its 32 k
+// of the step. live: the quarter lies inside K; xp: in the input part.
+template <int RB, int G>
+__device__ __forceinline__ void ksb_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KsLds As,
+                                         int buf, int rl, int kc, bool live, bool xp) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    if constexpr (NRB == 0) return;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    uint4 g[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) g[q] = *reinterpret_cast<const uint4 *>(&As[buf][16 * RB + 16 * q + rl][kc]);
+    bf8_t b[4];
+    b[0] = __builtin_bit_cast(bf8_t, g[0]);
+    b[1] = __builtin_bit_cast(bf8_t, g[1]);
+    b[2] = __builtin_bit_cast(bf8_t, xp ? g[2] : z);
+    b[3] = __builtin_bit_cast(bf8_t, xp ? z : g[2]);
+    bf8_t a[NRB > 0 ? NRB : 1];
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]);
+        a[i] = __builtin_bit_cast(bf8_t, live ? v : z);
+    }
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[q], acc[i][q], 0, 0, 0);
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void ksb_waves(KsLds As, float *smem, const KsEpi &ep, int a_r, int a_k, int a_c, int Kx,
+                                          int K, const uint16_t *bp0, const uint16_t *bp1, bool has_b1, int w,
+                                          int lane, int tid) {
+    constexpr int NPA = (16 * RB + 31) / 32;
+    constexpr int NRB = (RB - G + 1) / 2;
+    f4_t acc[NRB > 0 ? NRB : 1][4];   // [row block G + 2 i][reset, update, candidate input part, history part]
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = f4_t{0, 0, 0, 0};
+    const int rl = lane & 15, kc = 16 * (w & 3) + 4 * (lane >> 4);   // kc in floats: bf16 k = 32 (w % 4) + 8 (lane / 16)
+    const int ns = (K + KSB_BK - 1) / KSB_BK;                         // >= 1
+    // two register stages as in the fp32 tile: S0 carries the odd steps and
+    // S1 the even ones from step 2 on; LDS buffer s & 1 holds step s
+    KsbStage<NPA> S0, S1;
+    ksb_load<RB>(S0, ep.ptrs, a_r, a_k, min(1, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+    ksb_load<RB>(S1, ep.ptrs, a_r, a_k, min(2, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+    auto step = [&](int st, auto PARc) {
+        constexpr int PAR = decltype(PARc)::value;
+        const int kq = st * KSB_BK + 32 * (w & 3);   // wave-uniform
+        ksb_step<RB, G>(acc, As, PAR, rl, kc, kq < K, kq < Kx);
+        KsbStage<NPA> &St = PAR == 0 ? S0 : S1;
+        if (st + 1 < ns) ksb_store<RB>(St, As, 1 - PAR, a_r, a_c, has_b1);
+        // past the last step the stage re-reads the last step (unused), so
+        // that every step issues the same loads and the waits stay exact
+        ksb_load<RB>(St, ep.ptrs, a_r, a_k, min(st + 3, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+        __syncthreads();
+    };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    int st = 0;
+    for (; st + 1 < ns; st += 2) {
+        step(st, P0());
+        step(st + 1, P1());
+    }
+    if (st < ns) step(st, P0());
+    ks_gates<RB, G, 5>(acc, smem, ep, w, lane, tid);
+}
+
+template <int RB>
+__device__ __forceinline__ void gru_ks_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
+                                            int NR) {
+    constexpr int BM = 16 * RB;
+    constexpr int NPA = (BM + 31) / 32;
+    const int NU = d.H / KS_TU;
+    int rt, ut;
+    if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles (and their weights in its L2)
+        const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
+        rt = idx / per;
+        ut = xcd + 8 * (idx % per);
+    } else {
+        rt = tile / NU;
+        ut = tile % NU;
+    }
+    const int m0 = rt * BM, j0 = ut * KS_TU;
+    if (rt >= NR || m0 >= M) return;   // block-uniform
+
+    KsLds As = reinterpret_cast<KsLds>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KSB_PTRS);   // [BM][5]
+    float *hprev = smem + KSB_HPREV;                         // [BM][16]
+
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
     const int K = Kx + d.H;
     const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
 
     // the tile's row pointers (rows past M read row M - 1: their products
-    // only reach rows the epilogue skips)
-    if (tid < KB_BM) {
+    // only reach rows the epilogue skips): destination, fp32 h (this layer's
+    // part), bf16 h (this layer's part), bf16 x (embedding row, or the bf16
+    // copy of the first layer's h'), and where the first layer's tiles put
+    // that copy when there is a second layer
+    if (tid < BM) {
         const int m = min(m0 + tid, M - 1);
         const bool live = m0 + tid < M;
         ptrs[5 * tid] = live ? row_at(R, d.f_rowdst, m) : 0;
@@ -879,130 +833,51 @@ __device__ __forceinline__ void gru_kb_bf16(const Dev &d, const Rows &R, int lay
         ptrs[5 * tid + 4] = live && layer == 0 && d.L == 2 ? (u64)row_ptr(R, d.f_xbf, m, d.H) : 0;
     }
     __syncthreads();
-    // the epilogue's fp32 h: thread t, unit t % 32, rows t / 32 + 16 j
-#pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-        const int r = (tid >> 5) + 16 * jj;
-        hprev[r * KB_TU + (tid & 31)] = reinterpret_cast<const float *>(ptrs[5 * r + 1])[j0 + (tid & 31)];
-    }
-    // loaders: thread t, chunk t % 16 (8 k) of A rows t/16 + 32 j (j < 4) and
-    // weight rows t/16 + 32 j (j < 3): gate row / 32, unit row % 32
-    const int lr = tid >> 4, lc = (tid & 15) * 8;
-    const uint16_t *bp[3];
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-        const int br = lr + 32 * j;
-        bp[j] = Wp + (size_t)((br >> 5) * d.H + j0 + (br & 31)) * K;
-    }
-    auto load = [&](KbStage &S, int k0) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const u64 *pr = ptrs + 5 * (lr + 32 * j);
-            const int k = min(k0 + lc, K - 8);   // past K: an unused chunk, in bounds
-            const uint16_t *src = k < Kx ? reinterpret_cast<const uint16_t *>(pr[3]) + k
-                                         : reinterpret_cast<const uint16_t *>(pr[2]) + (k - Kx);
-            S.v[j] = ldg<uint4>(src);
-        }
-#pragma unroll
-        for (int j = 0; j < 3; ++j) S.v[4 + j] = ldg<uint4>(bp[j] + min(k0 + lc, K - 8));
-    };
-    auto store = [&](const KbStage &S, int buf) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4 *>(&As[buf][lr + 32 * j][lc]) = S.v[j];
-#pragma unroll
-        for (int j = 0; j < 3; ++j) *reinterpret_cast<uint4 *>(&As[buf][KB_BM + lr + 32 * j][lc]) = S.v[4 + j];
-    };
+    // A loader: rows tid/16 + 32 p, 8 consecutive k at 8 (tid % 16). B
+    // loader: weight rows tid/16 (and tid/16 + 32 for tid < 256): gate
+    // row / 16, unit row % 16. a_c: the chunk's LDS column in floats.
+    const int a_r = tid >> 4, a_k = (tid & 15) * 8, a_c = (tid & 15) * 4;
+    const uint16_t *bp0 = Wp + (size_t)((a_r >> 4) * d.H + j0 + (a_r & 15)) * K;   // row starts: the loads add k
+    const uint16_t *bp1 = Wp + (size_t)(2 * d.H + j0 + (a_r & 15)) * K;
+    const bool has_b1 = tid < 256;   // wave-uniform
 
-    const int rg = w & 3, kh = w >> 2;
-    f4_t acc[2][2][4];   // [row block rg + 4 i][unit block][reset, update, candidate input part, history part]
+    // step 0 into LDS, with the epilogue's fp32 h (the tile's 16 units of each
+    // row's history): thread (row i, unit u) for rows i = tid/16 + 32 p
+    const int hi = tid >> 4, hu = tid & 15;
+    float hv[NPA];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hv[p] = reinterpret_cast<const float *>(ptrs[5 * (hi + 32 * p) + 1])[j0 + hu];
+    KsEpi ep;
+    ep.ptrs = ptrs;
+    ep.hprev = hprev;
+    ep.j = j0 + hu;
+    ep.br = d.bl[ep.j];
+    ep.bz = d.bl[d.H + ep.j];
+    ep.bn = d.bl[2 * d.H + ep.j];
+    ep.lofs = (size_t)layer * d.H;
+    {
+        KsbStage<NPA> S;
+        ksb_load<RB>(S, ptrs, a_r, a_k, 0, Kx, K, bp0, bp1);
+        ksb_store<RB>(S, As, 0, a_r, a_c, has_b1);
+    }
 #pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) acc[i][u][g] = f4_t{0, 0, 0, 0};
-    // epilogue operands of the first K half's lanes: biases of their two units
-    float bias[2][3];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int g = 0; g < 3; ++g) bias[u][g] = kh == 0 ? d.bl[g * d.H + j0 + 16 * u + (lane & 15)] : 0.f;
-
-    // two register stages: the loads of step s + 2 are issued while step s
-    // multiplies; LDS buffer s & 1 holds step s
-    const int ns = (K + KB_BK - 1) / KB_BK;   // steps (the last may reach past K by 64)
-    KbStage S0, S1;
-    load(S0, 0);
-    store(S0, 0);
-    load(S0, KB_BK);
-    load(S1, 2 * KB_BK);
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hprev[(hi + 32 * p) * KS_TU + hu] = hv[p];
     __syncthreads();
-    // step s multiplies buffer s & 1, stores step s + 1 (held by S0 for even
-    // s, S1 for odd s) into the other buffer and loads step s + 3 into it
-    // (past the last step: an unused reload of the last step, so that every
-    // step issues the same loads and the waits stay exact)
-    auto step = [&](int st, auto PARc) {
-        constexpr int PAR = decltype(PARc)::value;
-        kb_mfma(acc, As[PAR], rg, kh, lane, st * KB_BK, Kx, K);
-        KbStage &S = PAR == 0 ? S0 : S1;
-        if (st + 1 < ns) store(S, 1 - PAR);
-        load(S, min(st + 3, ns - 1) * KB_BK);
-        __syncthreads();
-    };
-    using P0 = std::integral_constant<int, 0>;
-    using P1 = std::integral_constant<int, 1>;
-    int st = 0;
-    for (; st + 1 < ns; st += 2) {
-        step(st, P0());
-        step(st + 1, P1());
-    }
-    if (st < ns) step(st, P0());
-    // the second K half's partial sums through LDS (over the operand
-    // buffers), added in a fixed order by the first half's waves, which then
-    // apply the gates
-    f4_t *red = reinterpret_cast<f4_t *>(smem) + rg * (16 * 64);
-    if (kh == 1) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) red[((i * 2 + u) * 4 + g) * 64 + lane] = acc[i][u][g];
-    }
-    __syncthreads();
-    if (kh == 0) {
-        const size_t lofs = (size_t)layer * d.H;
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                f4_t s[4];
-#pragma unroll
-                for (int g = 0; g < 4; ++g) s[g] = acc[i][u][g] + red[((i * 2 + u) * 4 + g) * 64 + lane];
-                const int uu = 16 * u + (lane & 15), j = j0 + uu;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
-                    const int row = 16 * (rg + 4 * i) + 4 * (lane >> 4) + e;
-                    const u64 dp = ptrs[5 * row];
-                    if (dp) {
-                        const float rr = sigmoidf_(s[0][e] + bias[u][0]);
-                        const float z = sigmoidf_(s[1][e] + bias[u][1]);
-                        const float n = tanhf(s[2][e] + bias[u][2] + rr * s[3][e]);
-                        const float hn = (1.0f - z) * n + z * hprev[row * KB_TU + uu];
-                        reinterpret_cast<float *>(dp)[lofs + j] = hn;
-                        const u64 xp = ptrs[5 * row + 4];   // the next layer's bf16 input
-                        if (xp) reinterpret_cast<uint16_t *>(xp)[j] = f32_to_bf16(hn);
-                    }
-                }
-            }
-    }
+    if (w < 4) ksb_waves<RB, 0>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
+    else ksb_waves<RB, 1>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
     __syncthreads();   // LDS is reused by the next tile
+}
+
+template <bool BF16W, int RB>
+__device__ __forceinline__ void gru_ks(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile, int NR) {
+    if constexpr (BF16W) gru_ks_bf16<RB>(d, R, layer, M, smem, tile, NR);
+    else gru_ks_f32<RB>(d, R, layer, M, smem, tile, NR);
 }
 
 // One launch per layer; the device-side row count picks the path.
 static_assert(8 * N_TILES * 2 * 256 <= G_LDS_FLOATS, "narrow partial tiles exceed the LDS buffer");
-static_assert(8 * 64 * 16 <= G_LDS_FLOATS, "medium partial tiles exceed the LDS buffer");
 
 // ONE: the launch scores a single frame (the host knows), so the row lists
 // need no per-frame selection and the narrow path's operands can be loaded
@@ -1051,25 +926,20 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
             __syncthreads();
             gru_narrow<BF16W, false, N_TILES>(d, R, layer, M, smem, group(t), pre);
         }
-    } else if (M <= MD_MAXROWS) {     // 16-row MFMA tiles, K split over the waves
-        gru_medium<BF16W>(d, R, layer, M, smem);
-    } else if (BF16W) {               // 128 x 32-unit bf16 tiles, K split over two wave halves
-        const int ntiles = ((M + KB_BM - 1) / KB_BM) * (d.H / KB_TU);
-        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) gru_kb_bf16(d, R, layer, M, smem, t);
-    } else {                          // (16 RB) x 16-unit fp32 tiles, K split over the waves
+    } else {                          // (16 RB) x 16-unit tiles, K split over the waves
         const int NR = ks_row_tiles(d, M);
         const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
         const int ntiles = NR * (d.H / KS_TU);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
             switch (RB) {
-                case 1: gru_ks_f32<1>(d, R, layer, M, smem, t, NR); break;
-                case 2: gru_ks_f32<2>(d, R, layer, M, smem, t, NR); break;
-                case 3: gru_ks_f32<3>(d, R, layer, M, smem, t, NR); break;
-                case 4: gru_ks_f32<4>(d, R, layer, M, smem, t, NR); break;
-                case 5: gru_ks_f32<5>(d, R, layer, M, smem, t, NR); break;
-                case 6: gru_ks_f32<6>(d, R, layer, M, smem, t, NR); break;
-                case 7: gru_ks_f32<7>(d, R, layer, M, smem, t, NR); break;
-                default: gru_ks_f32<8>(d, R, layer, M, smem, t, NR); break;
+                case 1: gru_ks<BF16W, 1>(d, R, layer, M, smem, t, NR); break;
+                case 2: gru_ks<BF16W, 2>(d, R, layer, M, smem, t, NR); break;
+                case 3: gru_ks<BF16W, 3>(d, R, layer, M, smem, t, NR); break;
+                case 4: gru_ks<BF16W, 4>(d, R, layer, M, smem, t, NR); break;
+                case 5: gru_ks<BF16W, 5>(d, R, layer, M, smem, t, NR); break;
+                case 6: gru_ks<BF16W, 6>(d, R, layer, M, smem, t, NR); break;
+                case 7: gru_ks<BF16W, 7>(d, R, layer, M, smem, t, NR); break;
+                default: gru_ks<BF16W, 8>(d, R, layer, M, smem, t, NR); break;
             }
         }
     }

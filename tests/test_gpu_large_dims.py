@@ -1,8 +1,9 @@
 """Every GRU path at the Large model's shapes, against the oracle.
 
 A warm Large run has few new history keys per frame (Sec. 3: the history
-cache absorbs the rest), so most frames run the narrow (at most 32 rows) and
-medium (at most 256 rows) GRU paths, while cold frames run the tiled path.
+cache absorbs the rest), so most frames run the narrow path (at most 32
+rows) and the others the tiled path, whose row tiles shrink with the row
+count.
 Here each path runs at E = 512, H = 1024: one fp32 layer (K = 1536), and two
 bf16 layers (K = 1536, then 2048). A first frame puts some keys in the
 history cache; the frame under test then has exactly M new history keys,
@@ -39,7 +40,7 @@ def path_of(M, one):
         return "narrow_preloaded"
     if M <= 32:
         return "narrow"
-    return "medium" if M <= 256 else "tiled"
+    return "tiled"
 
 
 def cases():
