@@ -136,18 +136,17 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     u64 words[kWordsPerLane];
     bool bad = false;
     u64 hs = 0;
+    // the lane's row elements, kept for the GEMM's bf16 copy of the row:
+    // sign v[u] = element 64 u + lane; k digits float4 s = elements
+    // 4 (lane + 64 s) ..; exact float2 s = elements 2 (lane + 64 s) ..
+    static_assert(kSignWords <= 32 && 2 * kWordsPerLane <= 32, "row elements per lane");
+    __attribute__((aligned(16))) float rv[32];
     if (d.qmode == RNNLM_Q_SIGN) {
         // the whole row in flight at once (one coalesced load per 64
         // elements), then one ballot per code word
-        float v[kSignWords];
+        float *v = rv;
 #pragma unroll
         for (int u = 0; u < kSignWords; ++u) v[u] = u < CW ? ldg<float>(x + u * 64 + lane) : 0.0f;
-        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
-            uint16_t *hb = d.f_hbf + (size_t)i * d.LH;
-#pragma unroll
-            for (int u = 0; u < kSignWords; ++u)
-                if (u < CW) hb[u * 64 + lane] = f32_to_bf16(v[u]);
-        }
         words[0] = 0;
 #pragma unroll
         for (int u = 0; u < kSignWords; ++u) {
@@ -160,16 +159,10 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
         if (lane < CW) hs = mix64(words[0] ^ ((u64)(lane + 1) * kPhi));
     } else if (d.qmode == RNNLM_Q_SIGDIG) {
         // all of the row's loads first (4 elements per code word), then the codes
-        float4 v[kWordsPerLane / 2];
+        float4 *v = reinterpret_cast<float4 *>(rv);
 #pragma unroll
         for (int s = 0; s < kWordsPerLane / 2; ++s)
             v[s] = lane + 64 * s < CW ? ldg<float4>(x + 4 * (lane + 64 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
-        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
-            uint2 *hb = reinterpret_cast<uint2 *>(d.f_hbf + (size_t)i * d.LH);
-#pragma unroll
-            for (int s = 0; s < kWordsPerLane / 2; ++s)
-                if (lane + 64 * s < CW) hb[lane + 64 * s] = pack_bf16x4(v[s]);
-        }
 #pragma unroll
         for (int s = 0; s < kWordsPerLane / 2; ++s) {
             const int w = lane + 64 * s;
@@ -183,17 +176,10 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
         }
     } else {
         // all of the row's loads first (2 elements per code word), then the codes
-        float2 v[kWordsPerLane];
+        float2 *v = reinterpret_cast<float2 *>(rv);
 #pragma unroll
         for (int s = 0; s < kWordsPerLane; ++s)
             v[s] = lane + 64 * s < CW ? ldg<float2>(x + 2 * (lane + 64 * s)) : make_float2(0.f, 0.f);
-        if (d.wdtype == RNNLM_BF16) {   // the GEMM's bf16 copy of the row
-            uint32_t *hb = reinterpret_cast<uint32_t *>(d.f_hbf + (size_t)i * d.LH);
-#pragma unroll
-            for (int s = 0; s < kWordsPerLane; ++s)
-                if (lane + 64 * s < CW)
-                    hb[lane + 64 * s] = (uint32_t)f32_to_bf16(v[s].x) | ((uint32_t)f32_to_bf16(v[s].y) << 16);
-        }
 #pragma unroll
         for (int s = 0; s < kWordsPerLane; ++s) {
             const int w = lane + 64 * s;
@@ -244,6 +230,30 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
         }
         if (emp) break;
         base = (base + kProbeWin) & d.hi_mask;
+    }
+
+    // The GEMM's bf16 copy of the row, for a key the cache does not hold
+    // (only such a key can become a GRU row; hit is wave-uniform).
+    if (d.wdtype == RNNLM_BF16 && hit < 0) {
+        if (d.qmode == RNNLM_Q_SIGN) {
+            uint16_t *hb = d.f_hbf + (size_t)i * d.LH;
+#pragma unroll
+            for (int u = 0; u < kSignWords; ++u)
+                if (u < CW) hb[u * 64 + lane] = f32_to_bf16(rv[u]);
+        } else if (d.qmode == RNNLM_Q_SIGDIG) {
+            uint2 *hb = reinterpret_cast<uint2 *>(d.f_hbf + (size_t)i * d.LH);
+            const float4 *v = reinterpret_cast<const float4 *>(rv);
+#pragma unroll
+            for (int s = 0; s < kWordsPerLane / 2; ++s)
+                if (lane + 64 * s < CW) hb[lane + 64 * s] = pack_bf16x4(v[s]);
+        } else {
+            uint32_t *hb = reinterpret_cast<uint32_t *>(d.f_hbf + (size_t)i * d.LH);
+            const float2 *v = reinterpret_cast<const float2 *>(rv);
+#pragma unroll
+            for (int s = 0; s < kWordsPerLane; ++s)
+                if (lane + 64 * s < CW)
+                    hb[lane + 64 * s] = (uint32_t)f32_to_bf16(v[s].x) | ((uint32_t)f32_to_bf16(v[s].y) << 16);
+        }
     }
 
     // per-frame outputs
