@@ -388,7 +388,7 @@ __device__ __forceinline__ void gru_narrow(const Dev &d, const Rows &R, int laye
 constexpr int KS_TU = 16;            // hidden units per tile
 constexpr int KS_RBMAX = 8;          // 16-row blocks per tile at most
 constexpr int KS_BK = 64;            // K step
-constexpr int KS_LDA = KS_BK + 4;    // padded LDS row (floats)
+constexpr int KS_LDA = KS_BK + 8;    // padded LDS row (floats): 288 B, no bank conflicts for the fragment reads
 constexpr int KS_BROWS = 3 * KS_TU;  // weight rows per tile
 constexpr int KS_OPER = 2 * (16 * KS_RBMAX + KS_BROWS) * KS_LDA;   // two operand buffers (floats)
 constexpr int KS_PTRS = KS_OPER;     // per tile row: destination, history source, input source (u64 each)

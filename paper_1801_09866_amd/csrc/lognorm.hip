@@ -20,8 +20,9 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 // 32 rows each. 13 column tiles (208 rows) leave 962 vocabulary tiles at
 // V = 200,000: under two rounds over the 256 CUs, with little idle tail.
 // K advances 16 at a time through double-buffered LDS (32 at a time measured
-// slower: more registers live across the barrier).
-constexpr int LN_BM = 256, LN_NC = 13, LN_BN = 16 * LN_NC, LN_BK = 16, LN_LD = LN_BK + 4;
+// slower: more registers live across the barrier). LDS rows are 24 floats:
+// with 20 the fragment reads (16 rows, 16 bytes each) conflict in the banks.
+constexpr int LN_BM = 256, LN_NC = 13, LN_BN = 16 * LN_NC, LN_BK = 16, LN_LD = LN_BK + 8;
 static_assert(LN_BK == 16 && LN_BM == 256 && LN_BN > 128 && LN_BN <= 256,
               "loaders: 4 threads x 4 k per row, rows tid / 4 + 128 j");
 
