@@ -394,7 +394,7 @@ constexpr int KS_OPER = 2 * (16 * KS_RBMAX + KS_BROWS) * KS_LDA;   // two operan
 constexpr int KS_PTRS = KS_OPER;     // per tile row: destination, history source, input source (u64 each)
 constexpr int KS_HPREV = KS_PTRS + 16 * KS_RBMAX * 6;   // per tile row: h of the tile's 16 units
 static_assert(KS_HPREV + 16 * KS_RBMAX * KS_TU <= G_LDS_FLOATS, "fp32 tiles exceed the LDS buffer");
-static_assert(2 * 8 * 4 * 64 * 4 <= KS_OPER, "fp32 partial sums exceed the operand buffers");
+static_assert(2 * 4 * 3 * 4 * 64 * 4 <= KS_OPER, "partial sums exceed the operand buffers");
 
 typedef float (*KsLds)[16 * KS_RBMAX + KS_BROWS][KS_LDA];
 
@@ -473,50 +473,68 @@ struct KsEpi {
     size_t lofs;         // this layer's offset in a destination row
 };
 
-// The end of a tile, for a wave of row group G holding NRB row blocks' four
-// accumulators per gate part. Rounds of two row blocks (2p from group 0,
-// 2p + 1 from group 1): the waves write their partial sums, [area p & 1]
-// [group][K quarter][part][lane], over the operand buffers; thread (h, i, u)
-// then sums the four K quarters of row i, unit u of row block 2p + h in a
-// fixed order and applies the gates. NP: u64 pointers per tile row (the
-// destination first; with 5, the fifth is where the bf16 copy of h' goes for
-// the next layer, or 0).
+// The end of a tile, for the wave of row group G and K quarter q = w % 4,
+// which holds NRB row blocks' four accumulators (reset, update, candidate
+// input part, candidate history part). In one LDS round each wave stores the
+// partial sums of the blocks it does not finish, [group][block][other
+// quarter][part][lane], over the operand buffers; wave q then finishes its
+// group's block q (when it has one): the four quarters' partials are added
+// in quarter order (the same fixed order whichever wave finishes), and each
+// lane applies the gates to its four rows of one unit. NP: u64 pointers per
+// tile row (the destination first; with 5, the fifth is where the bf16 copy
+// of h' goes for the next layer, or 0).
 template <int RB, int G, int NP>
 __device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], float *smem,
                                          const KsEpi &ep, int w, int lane, int tid) {
     constexpr int NRB = (RB - G + 1) / 2;
-    const float *red = smem;
-    const int h = tid >> 8, ei = (tid >> 4) & 15, eu = tid & 15;
+    static_assert(NRB <= 4, "a group has at most four row blocks");
+    f4_t *red = reinterpret_cast<f4_t *>(smem);
+    const int q = w & 3;   // wave-uniform
+    // slot of block i's partial from quarter qq (qq != i), part g
+    auto slot = [](int i, int qq, int g) { return ((G * 4 + i) * 3 + (qq - (qq > i))) * 4 + g; };
 #pragma unroll
-    for (int p = 0; p < (RB + 1) / 2; ++p) {
-        if (p < NRB) {
-            float4 *r = reinterpret_cast<float4 *>(smem) + (((p & 1) * 2 + G) * 4 + (w & 3)) * (4 * 64);
+    for (int i = 0; i < NRB; ++i)
+        if (i != q)
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                r[g * 64 + lane] = make_float4(acc[p][g][0], acc[p][g][1], acc[p][g][2], acc[p][g][3]);
+            for (int g = 0; g < 4; ++g) red[slot(i, q, g) * 64 + lane] = acc[i][g];
+    __syncthreads();
+    (void)tid;
+    if (q >= NRB) return;   // wave-uniform: no block q in this group
+    // the wave's own partial of block q, picked by a branch per quarter so
+    // that the accumulators are only ever indexed by constants
+    f4_t sum[4];
+    auto finish = [&](auto QQc) {
+        constexpr int QQ = decltype(QQc)::value;
+        if constexpr (QQ < NRB) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                sum[g] = QQ == 0 ? acc[QQ][g] : red[slot(QQ, 0, g) * 64 + lane];
+#pragma unroll
+                for (int qq = 1; qq < 4; ++qq) sum[g] += qq == QQ ? acc[QQ][g] : red[slot(QQ, qq, g) * 64 + lane];
+            }
         }
-        __syncthreads();
-        const int rb = 2 * p + h;
-        if (rb < RB) {   // wave-uniform
-            // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
-            const float *rf = red + ((p & 1) * 2 + h) * (4 * 4 * 256) + (16 * (ei >> 2) + eu) * 4 + (ei & 3);
-            float sg[4] = {0.f, 0.f, 0.f, 0.f};
+    };
+    switch (q) {
+        case 0: finish(std::integral_constant<int, 0>()); break;
+        case 1: finish(std::integral_constant<int, 1>()); break;
+        case 2: finish(std::integral_constant<int, 2>()); break;
+        default: finish(std::integral_constant<int, 3>()); break;
+    }
+    // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+    const int eu = lane & 15;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) sg[g] += rf[(q * 4 + g) * 256];
-            const int row = 16 * rb + ei;
-            const u64 dp = ep.ptrs[NP * row];
-            if (dp) {
-                const float rr = sigmoidf_(sg[0] + ep.br);
-                const float z = sigmoidf_(sg[1] + ep.bz);
-                const float n = tanhf(sg[2] + ep.bn + rr * sg[3]);
-                const float hn = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
-                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
-                if constexpr (NP == 5) {
-                    const u64 xp = ep.ptrs[NP * row + 4];
-                    if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
-                }
+    for (int e = 0; e < 4; ++e) {
+        const int row = 16 * (G + 2 * q) + 4 * (lane >> 4) + e;
+        const u64 dp = ep.ptrs[NP * row];
+        if (dp) {
+            const float rr = sigmoidf_(sum[0][e] + ep.br);
+            const float z = sigmoidf_(sum[1][e] + ep.bz);
+            const float n = tanhf(sum[2][e] + ep.bn + rr * sum[3][e]);
+            const float hn = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
+            reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+            if constexpr (NP == 5) {
+                const u64 xp = ep.ptrs[NP * row + 4];
+                if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
             }
         }
     }
