@@ -42,64 +42,14 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
     const int w1 = key.x;
     const int t = key.w;
     const bool probe = rec.flags & QF_PROBE;   // wave-uniform: one query per wave
-    // Once the record is in, everything the query can need is loaded at
-    // once: the LM cache's first probe record (for a cached history key), the
-    // output row, the history row, the bias and the MaxEnt weights. A hit
-    // wastes the row loads but saves the round trip a miss would wait for.
-    // the LM cache's linear-probe sequence from the key's position, kProbeWin
-    // records at a time (lane l reads record l of the window)
+    // A query whose history key was cached first probes the LM cache (the
+    // linear-probe sequence from the key's position, kProbeWin records at a
+    // time, lane l reading record l of the window); only a miss then loads
+    // the output row, the history row, the bias and the MaxEnt weights.
+    // (Loading the rows alongside the probe was measured slower: the loads
+    // wasted on hits cost more than the round trip they save on misses.)
     unsigned base = (unsigned)(query_hash((u64)rec.hs, key.y, key.z, t) & d.si_mask);
     ScEnt e = d.sc_tab[probe ? (base + (lane & (kProbeWin - 1))) & d.si_mask : 0];
-    const float *h = reinterpret_cast<const float *>(rec.hptr);
-    float acc = 0.0f;
-    if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
-        const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
-        float4 a[kRowSteps], b[kRowSteps];
-#pragma unroll
-        for (int st = 0; st < kRowSteps; ++st) {
-            const int k = lane * 4 + st * 256;
-            a[st] = b[st] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (k < d.H) {
-                a[st] = ldg<float4>(u + k);
-                b[st] = ldg<float4>(h + k);
-            }
-        }
-#pragma unroll
-        for (int st = 0; st < kRowSteps; ++st) {
-            acc = fmaf(a[st].x, b[st].x, acc);
-            acc = fmaf(a[st].y, b[st].y, acc);
-            acc = fmaf(a[st].z, b[st].z, acc);
-            acc = fmaf(a[st].w, b[st].w, acc);
-        }
-    } else {   // 8 bf16 weights per lane per 512 elements
-        const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
-        uint4 a[kRowSteps / 2];
-        float4 b0[kRowSteps / 2], b1[kRowSteps / 2];
-#pragma unroll
-        for (int st = 0; st < kRowSteps / 2; ++st) {
-            const int k = lane * 8 + st * 512;
-            a[st] = make_uint4(0u, 0u, 0u, 0u);
-            b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (k < d.H) {
-                a[st] = ldg<uint4>(u + k);
-                b0[st] = ldg<float4>(h + k);
-                b1[st] = ldg<float4>(h + k + 4);
-            }
-        }
-#pragma unroll
-        for (int st = 0; st < kRowSteps / 2; ++st) {
-            acc = fmaf(__uint_as_float(a[st].x << 16), b0[st].x, acc);
-            acc = fmaf(__uint_as_float(a[st].x & 0xFFFF0000u), b0[st].y, acc);
-            acc = fmaf(__uint_as_float(a[st].y << 16), b0[st].z, acc);
-            acc = fmaf(__uint_as_float(a[st].y & 0xFFFF0000u), b0[st].w, acc);
-            acc = fmaf(__uint_as_float(a[st].z << 16), b1[st].x, acc);
-            acc = fmaf(__uint_as_float(a[st].z & 0xFFFF0000u), b1[st].y, acc);
-            acc = fmaf(__uint_as_float(a[st].w << 16), b1[st].z, acc);
-            acc = fmaf(__uint_as_float(a[st].w & 0xFFFF0000u), b1[st].w, acc);
-        }
-    }
-    float me = d.b_out[t];
-    for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)];
     bool hit = false;
     float s = 0.0f;
     if (probe) {   // the first matching record before the first empty one
@@ -118,6 +68,58 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
             base = (base + kProbeWin) & d.si_mask;
             e = d.sc_tab[(base + (lane & (kProbeWin - 1))) & d.si_mask];
         }
+    }
+    float acc = 0.0f, me = 0.0f;
+    if (!hit) {
+        const float *h = reinterpret_cast<const float *>(rec.hptr);
+        if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
+            const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
+            float4 a[kRowSteps], b[kRowSteps];
+#pragma unroll
+            for (int st = 0; st < kRowSteps; ++st) {
+                const int k = lane * 4 + st * 256;
+                a[st] = b[st] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (k < d.H) {
+                    a[st] = ldg<float4>(u + k);
+                    b[st] = ldg<float4>(h + k);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < kRowSteps; ++st) {
+                acc = fmaf(a[st].x, b[st].x, acc);
+                acc = fmaf(a[st].y, b[st].y, acc);
+                acc = fmaf(a[st].z, b[st].z, acc);
+                acc = fmaf(a[st].w, b[st].w, acc);
+            }
+        } else {   // 8 bf16 weights per lane per 512 elements
+            const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
+            uint4 a[kRowSteps / 2];
+            float4 b0[kRowSteps / 2], b1[kRowSteps / 2];
+#pragma unroll
+            for (int st = 0; st < kRowSteps / 2; ++st) {
+                const int k = lane * 8 + st * 512;
+                a[st] = make_uint4(0u, 0u, 0u, 0u);
+                b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (k < d.H) {
+                    a[st] = ldg<uint4>(u + k);
+                    b0[st] = ldg<float4>(h + k);
+                    b1[st] = ldg<float4>(h + k + 4);
+                }
+            }
+#pragma unroll
+            for (int st = 0; st < kRowSteps / 2; ++st) {
+                acc = fmaf(__uint_as_float(a[st].x << 16), b0[st].x, acc);
+                acc = fmaf(__uint_as_float(a[st].x & 0xFFFF0000u), b0[st].y, acc);
+                acc = fmaf(__uint_as_float(a[st].y << 16), b0[st].z, acc);
+                acc = fmaf(__uint_as_float(a[st].y & 0xFFFF0000u), b0[st].w, acc);
+                acc = fmaf(__uint_as_float(a[st].z << 16), b1[st].x, acc);
+                acc = fmaf(__uint_as_float(a[st].z & 0xFFFF0000u), b1[st].y, acc);
+                acc = fmaf(__uint_as_float(a[st].w << 16), b1[st].z, acc);
+                acc = fmaf(__uint_as_float(a[st].w & 0xFFFF0000u), b1[st].w, acc);
+            }
+        }
+        me = d.b_out[t];
+        for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)];
     }
     if (!hit) s = wave_sum(acc) + me;
     if (lane == 0) {
