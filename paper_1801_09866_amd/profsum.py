@@ -151,14 +151,26 @@ def sweep(a):
     g = a.group
     print("%-22s %5s %10s %12s %12s %9s" % ("kernel", "size", "us", "fetch_MB", "write_MB", "MfmaUtil"))
     for fam in sorted(dur):
-        n = len(dur[fam]) // g
+        # a launch of a kernel that runs once per layer is several dispatches:
+        # merge them (times and bytes summed, MfmaUtil averaged)
+        per = max(1, len(dur[fam]) // (a.sizes * g))
+
+        def merged(v, avg=False):
+            out = []
+            for k in range(0, len(v) - per + 1, per):
+                x = v[k:k + per]
+                out.append(sum(x) / len(x) if avg else sum(x))
+            return out
+        d_ = merged(dur[fam])
+        c_ = {c: merged(v, c == "MfmaUtil") for c, v in cnt[fam].items()}
+        n = len(d_) // g
         for s in range(n):
             sl = slice(s * g + 1, (s + 1) * g)
             mean = lambda v: sum(v[sl]) / len(v[sl]) if len(v) >= (s + 1) * g else float("nan")
-            us = mean(dur[fam]) / 1e3
-            fb = mean(cnt[fam]["FETCH_SIZE"]) * a.fetch_scale / 1e6 if cnt[fam].get("FETCH_SIZE") else float("nan")
-            wb = mean(cnt[fam]["WRITE_SIZE"]) * a.write_scale / 1e6 if cnt[fam].get("WRITE_SIZE") else float("nan")
-            mu = mean(cnt[fam]["MfmaUtil"]) if cnt[fam].get("MfmaUtil") else float("nan")
+            us = mean(d_) / 1e3
+            fb = mean(c_["FETCH_SIZE"]) * a.fetch_scale / 1e6 if c_.get("FETCH_SIZE") else float("nan")
+            wb = mean(c_["WRITE_SIZE"]) * a.write_scale / 1e6 if c_.get("WRITE_SIZE") else float("nan")
+            mu = mean(c_["MfmaUtil"]) if c_.get("MfmaUtil") else float("nan")
             print("%-22s %5d %10.2f %12.2f %12.2f %9.1f" % (fam, s, us, fb, wb, mu))
 
 
@@ -287,6 +299,7 @@ def main():
     ap.add_argument("--sweep-trace", default=None, help="saturation sweep: the kernel-trace run's directory")
     ap.add_argument("--mfma", default=None, help="saturation sweep: an MfmaUtil counter run's directory")
     ap.add_argument("--group", type=int, default=6, help="saturation sweep: launches per size")
+    ap.add_argument("--sizes", type=int, default=4, help="saturation sweep: number of sizes")
     ap.add_argument("--span", default=None, help="bench frames: the workload name for traffic lines")
     ap.add_argument("--trace", default=None, help="bench frames: the kernel-trace run's directory")
     ap.add_argument("--warmup", type=int, default=5)
