@@ -158,7 +158,10 @@ int rnnlm_create(const rnnlm_config *cfg, const rnnlm_weights *w, void *workspac
  * when its history key is cached). Asynchronous on `stream`. Only this call's
  * kernels read the frame's inputs (and, through hist_ptr, the rows it names):
  * once they have completed in stream order, the caller may reuse those
- * buffers, e.g. as the target of the next frame's host-to-device copy. */
+ * buffers, e.g. as the target of the next frame's host-to-device copy. The
+ * call only enqueues kernels (no allocation, memset or synchronisation), so
+ * a sequence of frames may be captured into a HIP graph and replayed from
+ * the same cache state (stage timing off). */
 int rnnlm_score_frame(rnnlm_t *ctx, const rnnlm_frame *frame, const rnnlm_out *out, void *stream);
 
 /* A block of independent frames in one set of launches (Sec. 4 batches a
