@@ -122,7 +122,10 @@ __device__ void fold_counts(const Dev &d, int npart) {
     }
 }
 
-// one wave: history i of a frame
+// one wave: history i of a frame. BF16: the model's GEMM takes bf16 rows, so
+// the wave also writes the row's bf16 copy (fp32 models keep no row elements
+// live across the cache probe, and more waves fit).
+template <bool BF16>
 __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, int i) {
     const int lane = threadIdx.x & 63;
     if (i >= f.n_hist) return;
@@ -140,7 +143,7 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     // sign v[u] = element 64 u + lane; k digits float4 s = elements
     // 4 (lane + 64 s) ..; exact float2 s = elements 2 (lane + 64 s) ..
     static_assert(kSignWords <= 32 && 2 * kWordsPerLane <= 32, "row elements per lane");
-    __attribute__((aligned(16))) float rv[32];
+    __attribute__((aligned(16))) float rv[32];   // registers: indexed only by constants
     if (d.qmode == RNNLM_Q_SIGN) {
         // the whole row in flight at once (one coalesced load per 64
         // elements), then one ballot per code word
@@ -234,7 +237,7 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
 
     // The GEMM's bf16 copy of the row, for a key the cache does not hold
     // (only such a key can become a GRU row; hit is wave-uniform).
-    if (d.wdtype == RNNLM_BF16 && hit < 0) {
+    if (BF16 && hit < 0) {
         if (d.qmode == RNNLM_Q_SIGN) {
             uint16_t *hb = d.f_hbf + (size_t)i * d.LH;
 #pragma unroll
@@ -391,7 +394,7 @@ __device__ void hist_block_sigdig(const Dev &d, const FrameArgs &f, const Decade
 // are split among the frames by the ranges in fb. MULTI = false (a single
 // frame) reads everything at fixed argument offsets, so no argument load
 // waits for another.
-template <bool MULTI>
+template <bool MULTI, bool BF16>
 __global__ __launch_bounds__(256) void k_hist_key(Dev d0, FrameBlock fb, DecadeTab T) {
     const int b = blockIdx.x, n = MULTI ? fb.n : 1;
     const int hb = MULTI ? fb.hoff[n] : fb.hoff[1], qb = MULTI ? fb.qoff[n] : fb.qoff[1],
@@ -418,7 +421,7 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d0, FrameBlock fb, DecadeT
     const FrameArgs &f = fb.f[e];
     if (role == 0) {
         if (d.qmode == RNNLM_Q_SIGDIG) hist_block_sigdig(d, f, T, lb);   // one block per history
-        else hist_wave(d, f, T, lb * 4 + wave_id());                    // one wave per history
+        else hist_wave<BF16>(d, f, T, lb * 4 + wave_id());              // one wave per history
     }
     else if (role == 1) query_key(d, f, lb * blockDim.x + threadIdx.x);
     else if (role == 2) insert_staged(d, lb, fb.soff[e + 1] - fb.soff[e]);
@@ -482,8 +485,13 @@ void launch_fold_stats(const Dev &d, const FoldParts &fp, hipStream_t s) {
 void launch_hist_key(const Dev &d, const FrameBlock &fb, const DecadeTab &T, hipStream_t s, Stamp ts) {
     const int n = fb.n;
     const unsigned grid = fb.hoff[n] + fb.qoff[n] + fb.soff[n] + n;
-    if (n > 1) launch_k(k_hist_key<true>, grid, 256, s, ts, d, fb, T);
-    else launch_k(k_hist_key<false>, grid, 256, s, ts, d, fb, T);
+    if (d.wdtype == RNNLM_BF16) {
+        if (n > 1) launch_k(k_hist_key<true, true>, grid, 256, s, ts, d, fb, T);
+        else launch_k(k_hist_key<false, true>, grid, 256, s, ts, d, fb, T);
+    } else {
+        if (n > 1) launch_k(k_hist_key<true, false>, grid, 256, s, ts, d, fb, T);
+        else launch_k(k_hist_key<false, false>, grid, 256, s, ts, d, fb, T);
+    }
 }
 void launch_debug_quantize(const float *x, long long n, int qmode, int k, const DecadeTab &T,
                            void *codes, int *err, hipStream_t s) {
