@@ -474,8 +474,8 @@ __device__ __forceinline__ void ks_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB -
 
 // What the epilogue of a tile needs besides the partial sums.
 struct KsEpi {
-    const u64 *ptrs;     // per tile row: destination (0 past M), history source, input source
-    const float *hprev;  // per tile row: h of the tile's 16 units
+    const u64 *ptrs;     // per tile row: destination first (0 past M), then the sources
+    const float *hprev;  // per tile row: h of the tile's units
     float br, bz, bn;    // this thread's unit's biases
     int j;               // this thread's unit
     size_t lofs;         // this layer's offset in a destination row
@@ -488,10 +488,8 @@ struct KsEpi {
 // quarter][part][lane], over the operand buffers; wave q then finishes its
 // group's block q (when it has one): the four quarters' partials are added
 // in quarter order (the same fixed order whichever wave finishes), and each
-// lane applies the gates to its four rows of one unit. NP: u64 pointers per
-// tile row (the destination first; with 5, the fifth is where the bf16 copy
-// of h' goes for the next layer, or 0).
-template <int RB, int G, int NP>
+// lane applies the gates to its four rows of one unit.
+template <int RB, int G>
 __device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], float *smem,
                                          const KsEpi &ep, int w, int lane, int tid) {
     constexpr int NRB = (RB - G + 1) / 2;
@@ -533,17 +531,13 @@ __device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int row = 16 * (G + 2 * q) + 4 * (lane >> 4) + e;
-        const u64 dp = ep.ptrs[NP * row];
+        const u64 dp = ep.ptrs[3 * row];
         if (dp) {
             const float rr = sigmoidf_(sum[0][e] + ep.br);
             const float z = sigmoidf_(sum[1][e] + ep.bz);
             const float n = tanhf(sum[2][e] + ep.bn + rr * sum[3][e]);
             const float hn = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
             reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
-            if constexpr (NP == 5) {
-                const u64 xp = ep.ptrs[NP * row + 4];
-                if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
-            }
         }
     }
 }
@@ -602,7 +596,7 @@ __device__ __forceinline__ void ks_waves(KsLds As, float *smem, const KsEpi &ep,
         step(kt + 1, Hh(), P1());
     }
     if (kt < nk) step(kt, Hh(), P0());
-    ks_gates<RB, G, 3>(acc, smem, ep, w, lane, tid);
+    ks_gates<RB, G>(acc, smem, ep, w, lane, tid);
 }
 
 template <int RB>
@@ -680,24 +674,6 @@ __device__ __forceinline__ void gru_ks_f32(const Dev &d, const Rows &R, int laye
     __syncthreads();   // LDS is reused by the next tile
 }
 
-// -------------------- tiled path (more than 32 rows): bf16 ------------------
-// The fp32 tile's shape and schedule (16 RB rows x 16 hidden units, 8 waves as
-// 2 row groups x 4 K quarters, double-buffered LDS, loads three steps ahead)
-// with bf16 operands: the history rows were rounded once per frame by the
-// keys kernel, and the second layer's input is the bf16 copy of the first
-// layer's h' that its tiles' epilogue writes. A step is 128 k, i.e. the same
-// 256 bytes per operand row as an fp32 step, so the LDS layout and every LDS
-// address are the fp32 tile's; a wave's quarter is 32 k, one 16 x 16 x 32 MFMA
-// per row block and gate part. A step may straddle the input / history
-// boundary or reach past K (E and H are multiples of 64): each 8-k chunk is
-// loaded from its own part (clamped inside K), and a wave's quarter, which
-// lies wholly in one part (or past K), feeds zeros to the candidate gate's
-// other accumulator (or to every product).
-constexpr int KSB_BK = 128;                               // K step (bf16 elements)
-constexpr int KSB_PTRS = KS_OPER;                         // per tile row: dst, h fp32, h bf16, x bf16, x copy dst
-constexpr int KSB_HPREV = KSB_PTRS + 16 * KS_RBMAX * 10;  // per tile row: h of the tile's 16 units
-static_assert(KSB_HPREV + 16 * KS_RBMAX * KS_TU <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
-
 // start of row m of a per-session per-row array of `stride` elements
 template <class T>
 __device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t stride) {
@@ -714,124 +690,198 @@ __device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t strid
     return shift_ptr(arr, o) + (size_t)(m - base) * stride;
 }
 
-template <int NPA>
-struct KsbStage {
-    uint4 a[NPA], b0, b1;
+// -------------------- tiled path (more than 32 rows): bf16 ------------------
+// 16 RB rows x 32 hidden units (96 weight rows) per tile, 64-k steps (128
+// bytes per operand row), double-buffered LDS and two register stages as in
+// the fp32 tile. E and H are multiples of 64, so a step lies wholly in the
+// input part or the history part. The 8 waves are 2 row groups x 2 unit
+// halves x 2 K halves: wave w = 4 g + 2 uh + kh takes row blocks g, g + 2,
+// ..., units 16 uh .. 16 uh + 15 of the tile and k = 32 kh .. 32 kh + 31 of
+// each step, one 16 x 16 x 32 MFMA per row block and gate. Waves w and w + 4
+// (one of each row group) share a SIMD. The history rows were rounded to
+// bf16 once per frame by the keys kernel, and the second layer's input is the
+// bf16 copy of the first layer's h' that its tiles' epilogue writes. Twice as
+// wide as the fp32 tile: a bf16 step's MFMAs are short, so each tile's fixed
+// cost (row pointers, first steps, gates) and each step's LDS round are
+// spread over twice the MFMA work, with half as many tiles.
+constexpr int KW_TU = 32;                                  // hidden units per tile
+constexpr int KW_BROWS = 3 * KW_TU;                        // weight rows per tile
+constexpr int KW_BK = 64;                                  // K step (bf16 elements)
+constexpr int KW_LDA = 40;                                 // LDS row (floats): 128 bytes of operands, 32 of padding
+constexpr int KW_ROWS = 16 * KS_RBMAX + KW_BROWS;
+constexpr int KW_OPER = 2 * KW_ROWS * KW_LDA;              // two operand buffers (floats)
+constexpr int KW_PTRS = KW_OPER;                           // per tile row: dst, h fp32, h bf16, x bf16, x copy dst
+constexpr int KW_HPREV = KW_PTRS + 16 * KS_RBMAX * 10;     // per tile row: h of the tile's 32 units
+static_assert(KW_HPREV + 16 * KS_RBMAX * KW_TU <= G_LDS_FLOATS, "wide bf16 tiles exceed the LDS buffer");
+static_assert(2 * 2 * 4 * 4 * 64 * 4 <= KW_OPER, "partial sums exceed the operand buffers");
+
+typedef float (*KwLds)[KW_ROWS][KW_LDA];
+
+// row tiles of the wide bf16 path for M rows (about one tile per CU)
+__device__ __forceinline__ int kw_row_tiles(const Dev &d, int M) {
+    const int NU = d.H / KW_TU;
+    const int R0 = max(1, 256 / NU);
+    return R0 * ((M + 128 * R0 - 1) / (128 * R0));
+}
+
+// A thread's share of one K step: 16-byte chunk t % 8 of A rows t / 8 and
+// t / 8 + 64 and of weight rows t / 8 and t / 8 + 64 (the second weight row
+// for t < 256 only: a tile has 96).
+struct KwStage {
+    uint4 a0, a1, b0, b1;
 };
 
-// Every thread issues the same loads, none behind a branch: a chunk past K
-// re-reads the last chunk inside K (its products are zeroed), rows past the
-// tile re-read its last row. bp0, bp1: the starts of the thread's weight rows.
+// Every thread issues the same loads: rows past the tile re-read its last
+// row, and a thread with no second weight row re-reads its first. bp0, bp1:
+// the thread's chunk of its weight rows at k = 0.
 template <int RB>
-__device__ __forceinline__ void ksb_load(KsbStage<(16 * RB + 31) / 32> &S, const u64 *ptrs, int a_r, int a_k, int k0,
-                                         int Kx, int K, const uint16_t *bp0, const uint16_t *bp1) {
-    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
-    const int k = min(k0 + a_k, K - 8);
-    const bool xp = k < Kx;
-#pragma unroll
-    for (int p = 0; p < NPA; ++p) {
-        const int row = min(a_r + 32 * p, BM - 1);
-        const uint16_t *src = reinterpret_cast<const uint16_t *>(ptrs[5 * row + (xp ? 3 : 2)]);
-        S.a[p] = ldg<uint4>(src + (xp ? k : k - Kx));
-    }
-    S.b0 = ldg<uint4>(bp0 + k);
-    S.b1 = ldg<uint4>(bp1 + k);
+__device__ __forceinline__ void kw_load(KwStage &S, const u64 *ptrs, int a_r, int a_c8, int k0, int Kx,
+                                        const uint16_t *bp0, const uint16_t *bp1) {
+    constexpr int BM = 16 * RB;
+    const bool xp = k0 < Kx;   // uniform: a step lies wholly in one part
+    const int ko = (xp ? k0 : k0 - Kx) + a_c8;
+    const int r0 = min(a_r, BM - 1), r1 = min(a_r + 64, BM - 1);
+    S.a0 = ldg<uint4>(reinterpret_cast<const uint16_t *>(ptrs[5 * r0 + (xp ? 3 : 2)]) + ko);
+    S.a1 = ldg<uint4>(reinterpret_cast<const uint16_t *>(ptrs[5 * r1 + (xp ? 3 : 2)]) + ko);
+    S.b0 = ldg<uint4>(bp0 + k0);
+    S.b1 = ldg<uint4>(bp1 + k0);
 }
 
 template <int RB>
-__device__ __forceinline__ void ksb_store(const KsbStage<(16 * RB + 31) / 32> &S, KsLds As, int buf, int a_r, int a_c,
-                                          bool has_b1) {
-    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
-#pragma unroll
-    for (int p = 0; p < NPA; ++p)
-        if (a_r + 32 * p < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r + 32 * p][a_c]) = S.a[p];
-    *reinterpret_cast<uint4 *>(&As[buf][BM + a_r][a_c]) = S.b0;
-    if (has_b1) *reinterpret_cast<uint4 *>(&As[buf][BM + 32 + a_r][a_c]) = S.b1;
+__device__ __forceinline__ void kw_store(const KwStage &S, KwLds As, int buf, int a_r, int a_cf, bool has_b1) {
+    constexpr int BM = 16 * RB;
+    if (a_r < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r][a_cf]) = S.a0;
+    if (a_r + 64 < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r + 64][a_cf]) = S.a1;
+    *reinterpret_cast<uint4 *>(&As[buf][BM + a_r][a_cf]) = S.b0;
+    if (has_b1) *reinterpret_cast<uint4 *>(&As[buf][BM + 64 + a_r][a_cf]) = S.b1;
 }
 
-// One K step of a wave of row group G: its row blocks G, G + 2, ... x
-// (reset, update, candidate input part, candidate history part) over its 32 k
-// of the step. live: the quarter lies inside K; xp: in the input part. mid()
-// runs after the first row block's MFMAs (before them with one row block), as
-// in the fp32 step.
-template <int RB, int G, class MID>
-__device__ __forceinline__ void ksb_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KsLds As,
-                                         int buf, int rl, int kc, bool live, bool xp, MID mid) {
+// One K step of a wave of row group G and unit half uh: its row blocks G, G +
+// 2, ... x (reset, update, candidate) over its 32 k of the step. NG: the
+// candidate gate's accumulator (2: input part, 3: history part). mid() runs
+// after the first row block's MFMAs (before them with one row block).
+template <int RB, int G, int NG, class MID>
+__device__ __forceinline__ void kw_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KwLds As,
+                                        int buf, int rl, int kc, int uh, MID mid) {
     constexpr int NRB = (RB - G + 1) / 2;
     if constexpr (NRB == 0) {
         mid();
         return;
     }
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    uint4 g[3];
+    bf8_t b[3];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) g[q] = *reinterpret_cast<const uint4 *>(&As[buf][16 * RB + 16 * q + rl][kc]);
-    bf8_t b[4];
-    b[0] = __builtin_bit_cast(bf8_t, g[0]);
-    b[1] = __builtin_bit_cast(bf8_t, g[1]);
-    b[2] = __builtin_bit_cast(bf8_t, xp ? g[2] : z);
-    b[3] = __builtin_bit_cast(bf8_t, xp ? z : g[2]);
+    for (int q = 0; q < 3; ++q)
+        b[q] = __builtin_bit_cast(bf8_t, *reinterpret_cast<const uint4 *>(&As[buf][16 * RB + 32 * q + 16 * uh + rl][kc]));
     bf8_t a[NRB > 0 ? NRB : 1];
 #pragma unroll
+    for (int i = 0; i < NRB; ++i)
+        a[i] = __builtin_bit_cast(bf8_t, *reinterpret_cast<const uint4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]));
+#pragma unroll
     for (int i = 0; i < NRB; ++i) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]);
-        a[i] = __builtin_bit_cast(bf8_t, live ? v : z);
+        if (i == 1 || NRB == 1) mid();
+        acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[0], acc[i][0], 0, 0, 0);
+        acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[1], acc[i][1], 0, 0, 0);
+        acc[i][NG] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[2], acc[i][NG], 0, 0, 0);
     }
+}
+
+// The end of a wide tile, for the wave of row group G, unit half uh and K
+// half kh. Each wave stores the partial sums of the row blocks the other K
+// half finishes ([group][unit half][block][part][lane], over the operand
+// buffers); after one barrier the wave of K half i % 2 finishes block i: its
+// partial plus the other half's (two terms, so the sum is the same whichever
+// wave adds them), and each lane applies the gates to its four rows of one
+// unit.
+template <int RB, int G>
+__device__ __forceinline__ void kw_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4],
+                                         float *smem, const KsEpi &ep, int uh, int kh, int lane) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    static_assert(NRB <= 4, "a group has at most four row blocks");
+    f4_t *red = reinterpret_cast<f4_t *>(smem);
+    auto slot = [&](int i, int g) { return (((G * 2 + uh) * 4 + i) * 4 + g) * 64 + lane; };
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+        if ((i & 1) != kh)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) red[slot(i, g)] = acc[i][g];
+    __syncthreads();
+    const int eu = lane & 15;
 #pragma unroll
     for (int i = 0; i < NRB; ++i) {
-        if (i == 1 || (NRB == 1 && i == 0)) mid();
+        if ((i & 1) != kh) continue;   // wave-uniform
+        f4_t sum[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[q], acc[i][q], 0, 0, 0);
+        for (int g = 0; g < 4; ++g) sum[g] = acc[i][g] + red[slot(i, g)];
+        // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = 16 * (G + 2 * i) + 4 * (lane >> 4) + e;
+            const u64 dp = ep.ptrs[5 * row];
+            if (dp) {
+                const float rr = sigmoidf_(sum[0][e] + ep.br);
+                const float z = sigmoidf_(sum[1][e] + ep.bz);
+                const float n = tanhf(sum[2][e] + ep.bn + rr * sum[3][e]);
+                const float hn = (1.0f - z) * n + z * ep.hprev[row * KW_TU + 16 * uh + eu];
+                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+                const u64 xp = ep.ptrs[5 * row + 4];
+                if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
+            }
+        }
     }
 }
 
 template <int RB, int G>
-__device__ __forceinline__ void ksb_waves(KsLds As, float *smem, const KsEpi &ep, int a_r, int a_k, int a_c, int Kx,
-                                          int K, const uint16_t *bp0, const uint16_t *bp1, bool has_b1, int w,
-                                          int lane, int tid) {
-    constexpr int NPA = (16 * RB + 31) / 32;
+__device__ __forceinline__ void kw_waves(KwLds As, float *smem, const KsEpi &ep, int a_r, int a_c8, int a_cf,
+                                         int Kx, int K, const uint16_t *bp0, const uint16_t *bp1, bool has_b1,
+                                         int w, int lane) {
     constexpr int NRB = (RB - G + 1) / 2;
     f4_t acc[NRB > 0 ? NRB : 1][4];   // [row block G + 2 i][reset, update, candidate input part, history part]
 #pragma unroll
     for (int i = 0; i < NRB; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) acc[i][q] = f4_t{0, 0, 0, 0};
-    const int rl = lane & 15, kc = 16 * (w & 3) + 4 * (lane >> 4);   // kc in floats: bf16 k = 32 (w % 4) + 8 (lane / 16)
-    const int ns = (K + KSB_BK - 1) / KSB_BK;                         // >= 1
-    // two register stages as in the fp32 tile: S0 carries the odd steps and
-    // S1 the even ones from step 2 on; LDS buffer s & 1 holds step s
-    KsbStage<NPA> S0, S1;
-    ksb_load<RB>(S0, ep.ptrs, a_r, a_k, min(1, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
-    ksb_load<RB>(S1, ep.ptrs, a_r, a_k, min(2, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
-    auto step = [&](int st, auto PARc) {
-        constexpr int PAR = decltype(PARc)::value;
-        const int kq = st * KSB_BK + 32 * (w & 3);   // wave-uniform
-        KsbStage<NPA> &St = PAR == 0 ? S0 : S1;
-        ksb_step<RB, G>(acc, As, PAR, rl, kc, kq < K, kq < Kx, [&] {
-            if (st + 1 < ns) ksb_store<RB>(St, As, 1 - PAR, a_r, a_c, has_b1);
+    const int uh = (w >> 1) & 1, kh = w & 1;
+    const int rl = lane & 15, kc = 16 * kh + 4 * (lane >> 4);   // kc in floats: bf16 k = 32 kh + 8 (lane / 16)
+    const int nk = K / KW_BK, nx = Kx / KW_BK;                    // nk >= 2
+    // S0 carries the odd steps and S1 the even ones from step 2 on; LDS
+    // buffer s & 1 holds step s (step 0 is in LDS already)
+    KwStage S0, S1;
+    kw_load<RB>(S0, ep.ptrs, a_r, a_c8, KW_BK, Kx, bp0, bp1);
+    kw_load<RB>(S1, ep.ptrs, a_r, a_c8, min(2, nk - 1) * KW_BK, Kx, bp0, bp1);
+    auto step = [&](int kt, auto NGc, auto PARc) {
+        constexpr int NG = decltype(NGc)::value, PAR = decltype(PARc)::value;
+        KwStage &St = PAR == 0 ? S0 : S1;
+        kw_step<RB, G, NG>(acc, As, PAR, rl, kc, uh, [&] {
+            if (kt + 1 < nk) kw_store<RB>(St, As, 1 - PAR, a_r, a_cf, has_b1);
         });
-        // past the last step the stage re-reads the last step (unused), so
-        // that every step issues the same loads and the waits stay exact
-        ksb_load<RB>(St, ep.ptrs, a_r, a_k, min(st + 3, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+        // past the last step the stage re-reads the last step (unused)
+        kw_load<RB>(St, ep.ptrs, a_r, a_c8, min(kt + 3, nk - 1) * KW_BK, Kx, bp0, bp1);
         __syncthreads();
     };
+    using X = std::integral_constant<int, 2>;
+    using Hh = std::integral_constant<int, 3>;
     using P0 = std::integral_constant<int, 0>;
     using P1 = std::integral_constant<int, 1>;
-    int st = 0;
-    for (; st + 1 < ns; st += 2) {
-        step(st, P0());
-        step(st + 1, P1());
+    int kt = 0;
+    for (; kt + 1 < nx; kt += 2) {
+        step(kt, X(), P0());
+        step(kt + 1, X(), P1());
     }
-    if (st < ns) step(st, P0());
-    ks_gates<RB, G, 5>(acc, smem, ep, w, lane, tid);
+    if (kt < nx) step(kt++, X(), P0());
+    if (kt & 1) step(kt++, Hh(), P1());
+    for (; kt + 1 < nk; kt += 2) {
+        step(kt, Hh(), P0());
+        step(kt + 1, Hh(), P1());
+    }
+    if (kt < nk) step(kt, Hh(), P0());
+    kw_gates<RB, G>(acc, smem, ep, uh, kh, lane);
 }
 
 template <int RB>
-__device__ __forceinline__ void gru_ks_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
+__device__ __forceinline__ void gru_kw_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
                                             int NR) {
     constexpr int BM = 16 * RB;
-    constexpr int NPA = (BM + 31) / 32;
-    const int NU = d.H / KS_TU;
+    const int NU = d.H / KW_TU;
     int rt, ut;
     if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles (and their weights in its L2)
         const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
@@ -841,12 +891,12 @@ __device__ __forceinline__ void gru_ks_bf16(const Dev &d, const Rows &R, int lay
         rt = tile / NU;
         ut = tile % NU;
     }
-    const int m0 = rt * BM, j0 = ut * KS_TU;
+    const int m0 = rt * BM, j0 = ut * KW_TU;
     if (rt >= NR || m0 >= M) return;   // block-uniform
 
-    KsLds As = reinterpret_cast<KsLds>(smem);
-    u64 *ptrs = reinterpret_cast<u64 *>(smem + KSB_PTRS);   // [BM][5]
-    float *hprev = smem + KSB_HPREV;                         // [BM][16]
+    KwLds As = reinterpret_cast<KwLds>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KW_PTRS);   // [BM][5]
+    float *hprev = smem + KW_HPREV;                         // [BM][32]
 
     const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
     const int Kx = layer == 0 ? d.E : d.H;
@@ -870,47 +920,260 @@ __device__ __forceinline__ void gru_ks_bf16(const Dev &d, const Rows &R, int lay
         ptrs[5 * tid + 4] = live && layer == 0 && d.L == 2 ? (u64)row_ptr(R, d.f_xbf, m, d.H) : 0;
     }
     __syncthreads();
-    // A loader: rows tid/16 + 32 p, 8 consecutive k at 8 (tid % 16). B
-    // loader: weight rows tid/16 (and tid/16 + 32 for tid < 256): gate
-    // row / 16, unit row % 16. a_c: the chunk's LDS column in floats.
-    const int a_r = tid >> 4, a_k = (tid & 15) * 8, a_c = (tid & 15) * 4;
-    const uint16_t *bp0 = Wp + (size_t)((a_r >> 4) * d.H + j0 + (a_r & 15)) * K;   // row starts: the loads add k
-    const uint16_t *bp1 = Wp + (size_t)(2 * d.H + j0 + (a_r & 15)) * K;
+    // loaders: rows tid / 8 (+ 64), chunk tid % 8 (8 bf16 = 4 floats of an
+    // LDS row); weight row b of the tile is gate b / 32, unit b % 32
+    const int a_r = tid >> 3, a_c8 = (tid & 7) * 8, a_cf = (tid & 7) * 4;
     const bool has_b1 = tid < 256;   // wave-uniform
+    const uint16_t *bp0 = Wp + (size_t)((a_r >> 5) * d.H + j0 + (a_r & 31)) * K + a_c8;
+    const uint16_t *bp1 = has_b1 ? Wp + (size_t)(2 * d.H + j0 + a_r) * K + a_c8 : bp0;
 
-    // step 0 into LDS, with the epilogue's fp32 h (the tile's 16 units of each
-    // row's history): thread (row i, unit u) for rows i = tid/16 + 32 p
-    const int hi = tid >> 4, hu = tid & 15;
-    float hv[NPA];
+    // step 0 into LDS, with the epilogue's fp32 h (the tile's 32 units of
+    // each row's history): thread (row tid / 32 + 16 p, unit tid % 32)
+    const int hi = tid >> 5, hu = tid & 31;
+    float hv[RB];
 #pragma unroll
-    for (int p = 0; p < NPA; ++p)
-        if (hi + 32 * p < BM) hv[p] = reinterpret_cast<const float *>(ptrs[5 * (hi + 32 * p) + 1])[j0 + hu];
+    for (int p = 0; p < RB; ++p) hv[p] = reinterpret_cast<const float *>(ptrs[5 * (hi + 16 * p) + 1])[j0 + hu];
     KsEpi ep;
     ep.ptrs = ptrs;
     ep.hprev = hprev;
-    ep.j = j0 + hu;
+    ep.j = j0 + 16 * ((w >> 1) & 1) + (lane & 15);
     ep.br = d.bl[ep.j];
     ep.bz = d.bl[d.H + ep.j];
     ep.bn = d.bl[2 * d.H + ep.j];
     ep.lofs = (size_t)layer * d.H;
     {
-        KsbStage<NPA> S;
-        ksb_load<RB>(S, ptrs, a_r, a_k, 0, Kx, K, bp0, bp1);
-        ksb_store<RB>(S, As, 0, a_r, a_c, has_b1);
+        KwStage S;
+        kw_load<RB>(S, ptrs, a_r, a_c8, 0, Kx, bp0, bp1);
+        kw_store<RB>(S, As, 0, a_r, a_cf, has_b1);
     }
 #pragma unroll
-    for (int p = 0; p < NPA; ++p)
-        if (hi + 32 * p < BM) hprev[(hi + 32 * p) * KS_TU + hu] = hv[p];
+    for (int p = 0; p < RB; ++p) hprev[(hi + 16 * p) * KW_TU + hu] = hv[p];
     __syncthreads();
-    if (w < 4) ksb_waves<RB, 0>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
-    else ksb_waves<RB, 1>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
+    if (w < 4) kw_waves<RB, 0>(As, smem, ep, a_r, a_c8, a_cf, Kx, K, bp0, bp1, has_b1, w, lane);
+    else kw_waves<RB, 1>(As, smem, ep, a_r, a_c8, a_cf, Kx, K, bp0, bp1, has_b1, w, lane);
     __syncthreads();   // LDS is reused by the next tile
 }
 
-template <bool BF16W, int RB>
-__device__ __forceinline__ void gru_ks(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile, int NR) {
-    if constexpr (BF16W) gru_ks_bf16<RB>(d, R, layer, M, smem, tile, NR);
-    else gru_ks_f32<RB>(d, R, layer, M, smem, tile, NR);
+// Many rows (more than one 32-unit tile per CU): tiles of 16 RB rows x 64
+// hidden units (192 weight rows), 64-k steps, the same loaders and LDS rows.
+// Wave w = 4 g + uq takes row blocks g, g + 2, ... and units 16 uq .. + 15
+// over the whole step (two 16 x 16 x 32 MFMAs per row block and gate), so the
+// gates need no partial sums from other waves. Half as many tiles again, each
+// with twice the MFMA work per step: 13-25% faster than 32-unit tiles at
+// 2048-16384 rows, but slower while 32-unit tiles still make one per CU
+// (their LDS traffic per MFMA is lower).
+constexpr int KQ_TU = 64;
+constexpr int KQ_BROWS = 3 * KQ_TU;
+constexpr int KQ_ROWS = 16 * KS_RBMAX + KQ_BROWS;
+constexpr int KQ_OPER = 2 * KQ_ROWS * KW_LDA;
+constexpr int KQ_PTRS = KQ_OPER;
+constexpr int KQ_HPREV = KQ_PTRS + 16 * KS_RBMAX * 10;
+static_assert(KQ_HPREV + 16 * KS_RBMAX * KQ_TU <= G_LDS_FLOATS, "64-unit bf16 tiles exceed the LDS buffer");
+typedef float (*KqLds)[KQ_ROWS][KW_LDA];
+
+__device__ __forceinline__ int kq_row_tiles(const Dev &d, int M) {
+    const int NU = d.H / KQ_TU;
+    const int R0 = max(1, 256 / NU);
+    return R0 * ((M + 128 * R0 - 1) / (128 * R0));
+}
+
+// A thread's share of one K step: 16-byte chunk t % 8 of A rows t / 8 and
+// t / 8 + 64 and of weight rows t / 8, t / 8 + 64, t / 8 + 128 (gate 0, 1, 2
+// of unit t / 8).
+struct KqStage {
+    uint4 a0, a1, b0, b1, b2;
+};
+
+template <int RB>
+__device__ __forceinline__ void kq_load(KqStage &S, const u64 *ptrs, int a_r, int a_c8, int k0, int Kx,
+                                        const uint16_t *bp, size_t bstride) {
+    constexpr int BM = 16 * RB;
+    const bool xp = k0 < Kx;
+    const int ko = (xp ? k0 : k0 - Kx) + a_c8;
+    const int r0 = min(a_r, BM - 1), r1 = min(a_r + 64, BM - 1);
+    S.a0 = ldg<uint4>(reinterpret_cast<const uint16_t *>(ptrs[5 * r0 + (xp ? 3 : 2)]) + ko);
+    S.a1 = ldg<uint4>(reinterpret_cast<const uint16_t *>(ptrs[5 * r1 + (xp ? 3 : 2)]) + ko);
+    S.b0 = ldg<uint4>(bp + k0);
+    S.b1 = ldg<uint4>(bp + bstride + k0);
+    S.b2 = ldg<uint4>(bp + 2 * bstride + k0);
+}
+
+template <int RB>
+__device__ __forceinline__ void kq_store(const KqStage &S, KqLds As, int buf, int a_r, int a_cf) {
+    constexpr int BM = 16 * RB;
+    if (a_r < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r][a_cf]) = S.a0;
+    if (a_r + 64 < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r + 64][a_cf]) = S.a1;
+    *reinterpret_cast<uint4 *>(&As[buf][BM + a_r][a_cf]) = S.b0;
+    *reinterpret_cast<uint4 *>(&As[buf][BM + 64 + a_r][a_cf]) = S.b1;
+    *reinterpret_cast<uint4 *>(&As[buf][BM + 128 + a_r][a_cf]) = S.b2;
+}
+
+template <int RB, int G, int NG, class MID>
+__device__ __forceinline__ void kq_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KqLds As,
+                                        int buf, int rl, int kc, int uq, MID mid) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    if constexpr (NRB == 0) {
+        mid();
+        return;
+    }
+    bf8_t b[2][3];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+            b[h][q] = __builtin_bit_cast(
+                bf8_t, *reinterpret_cast<const uint4 *>(&As[buf][16 * RB + 64 * q + 16 * uq + rl][kc + 16 * h]));
+    bf8_t a[NRB > 0 ? NRB : 1][2];
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            a[i][h] = __builtin_bit_cast(bf8_t, *reinterpret_cast<const uint4 *>(&As[buf][16 * (G + 2 * i) + rl][kc + 16 * h]));
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+        if (i == 1 || NRB == 1) mid();
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i][h], b[h][0], acc[i][0], 0, 0, 0);
+            acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i][h], b[h][1], acc[i][1], 0, 0, 0);
+            acc[i][NG] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i][h], b[h][2], acc[i][NG], 0, 0, 0);
+        }
+    }
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void kq_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4],
+                                         const KsEpi &ep, int uq, int lane) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    const int eu = lane & 15;
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = 16 * (G + 2 * i) + 4 * (lane >> 4) + e;
+            const u64 dp = ep.ptrs[5 * row];
+            if (dp) {
+                const float rr = sigmoidf_(acc[i][0][e] + ep.br);
+                const float z = sigmoidf_(acc[i][1][e] + ep.bz);
+                const float n = tanhf(acc[i][2][e] + ep.bn + rr * acc[i][3][e]);
+                const float hn = (1.0f - z) * n + z * ep.hprev[row * KQ_TU + 16 * uq + eu];
+                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+                const u64 xp = ep.ptrs[5 * row + 4];
+                if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
+            }
+        }
+    }
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void kq_waves(KqLds As, const KsEpi &ep, int a_r, int a_c8, int a_cf, int Kx, int K,
+                                         const uint16_t *bp, size_t bstride, int w, int lane) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    f4_t acc[NRB > 0 ? NRB : 1][4];
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = f4_t{0, 0, 0, 0};
+    const int uq = w & 3;
+    const int rl = lane & 15, kc = 4 * (lane >> 4);
+    const int nk = K / KW_BK, nx = Kx / KW_BK;
+    KqStage S0, S1;
+    kq_load<RB>(S0, ep.ptrs, a_r, a_c8, KW_BK, Kx, bp, bstride);
+    kq_load<RB>(S1, ep.ptrs, a_r, a_c8, min(2, nk - 1) * KW_BK, Kx, bp, bstride);
+    auto step = [&](int kt, auto NGc, auto PARc) {
+        constexpr int NG = decltype(NGc)::value, PAR = decltype(PARc)::value;
+        KqStage &St = PAR == 0 ? S0 : S1;
+        kq_step<RB, G, NG>(acc, As, PAR, rl, kc, uq, [&] {
+            if (kt + 1 < nk) kq_store<RB>(St, As, 1 - PAR, a_r, a_cf);
+        });
+        kq_load<RB>(St, ep.ptrs, a_r, a_c8, min(kt + 3, nk - 1) * KW_BK, Kx, bp, bstride);
+        __syncthreads();
+    };
+    using X = std::integral_constant<int, 2>;
+    using Hh = std::integral_constant<int, 3>;
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    int kt = 0;
+    for (; kt + 1 < nx; kt += 2) {
+        step(kt, X(), P0());
+        step(kt + 1, X(), P1());
+    }
+    if (kt < nx) step(kt++, X(), P0());
+    if (kt & 1) step(kt++, Hh(), P1());
+    for (; kt + 1 < nk; kt += 2) {
+        step(kt, Hh(), P0());
+        step(kt + 1, Hh(), P1());
+    }
+    if (kt < nk) step(kt, Hh(), P0());
+    kq_gates<RB, G>(acc, ep, uq, lane);
+}
+
+template <int RB>
+__device__ __forceinline__ void gru_kq_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
+                                            int NR) {
+    constexpr int BM = 16 * RB;
+    const int NU = d.H / KQ_TU;
+    int rt, ut;
+    if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles
+        const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
+        rt = idx / per;
+        ut = xcd + 8 * (idx % per);
+    } else {
+        rt = tile / NU;
+        ut = tile % NU;
+    }
+    const int m0 = rt * BM, j0 = ut * KQ_TU;
+    if (rt >= NR || m0 >= M) return;
+
+    KqLds As = reinterpret_cast<KqLds>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KQ_PTRS);
+    float *hprev = smem + KQ_HPREV;
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H;
+    const int K = Kx + d.H;
+    const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
+    // the tile's row pointers, as for the 32-unit tiles
+    if (tid < BM) {
+        const int m = min(m0 + tid, M - 1);
+        const bool live = m0 + tid < M;
+        ptrs[5 * tid] = live ? row_at(R, d.f_rowdst, m) : 0;
+        ptrs[5 * tid + 1] = row_at(R, d.f_rowh, m) + (u64)layer * d.H * 4;
+        ptrs[5 * tid + 2] = row_at(R, d.f_rowhb, m) + (u64)layer * d.H * 2;
+        ptrs[5 * tid + 3] = layer == 0 ? (u64)(reinterpret_cast<const uint16_t *>(d.emb) +
+                                               (size_t)(unsigned)row_at(R, d.f_roww, m) * d.E)
+                                       : (u64)row_ptr(R, d.f_xbf, m, d.H);
+        ptrs[5 * tid + 4] = live && layer == 0 && d.L == 2 ? (u64)row_ptr(R, d.f_xbf, m, d.H) : 0;
+    }
+    __syncthreads();
+    // weight rows a_r, a_r + 64, a_r + 128 of the tile: gate 0, 1, 2 of unit a_r
+    const int a_r = tid >> 3, a_c8 = (tid & 7) * 8, a_cf = (tid & 7) * 4;
+    const uint16_t *bp = Wp + (size_t)(j0 + a_r) * K + a_c8;
+    const size_t bstride = (size_t)d.H * K;
+    // step 0 into LDS, with the epilogue's fp32 h: thread (row tid / 64 + 8 p,
+    // unit tid % 64)
+    const int hi = tid >> 6, hu = tid & 63;
+    float hv[2 * RB];
+#pragma unroll
+    for (int p = 0; p < 2 * RB; ++p) hv[p] = reinterpret_cast<const float *>(ptrs[5 * (hi + 8 * p) + 1])[j0 + hu];
+    KsEpi ep;
+    ep.ptrs = ptrs;
+    ep.hprev = hprev;
+    ep.j = j0 + 16 * (w & 3) + (lane & 15);
+    ep.br = d.bl[ep.j];
+    ep.bz = d.bl[d.H + ep.j];
+    ep.bn = d.bl[2 * d.H + ep.j];
+    ep.lofs = (size_t)layer * d.H;
+    {
+        KqStage S;
+        kq_load<RB>(S, ptrs, a_r, a_c8, 0, Kx, bp, bstride);
+        kq_store<RB>(S, As, 0, a_r, a_cf);
+    }
+#pragma unroll
+    for (int p = 0; p < 2 * RB; ++p) hprev[(hi + 8 * p) * KQ_TU + hu] = hv[p];
+    __syncthreads();
+    if (w < 4) kq_waves<RB, 0>(As, ep, a_r, a_c8, a_cf, Kx, K, bp, bstride, w, lane);
+    else kq_waves<RB, 1>(As, ep, a_r, a_c8, a_cf, Kx, K, bp, bstride, w, lane);
+    __syncthreads();
 }
 
 // One launch per layer; the device-side row count picks the path.
@@ -963,20 +1226,56 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
             __syncthreads();
             gru_narrow<BF16W, false, N_TILES>(d, R, layer, M, smem, group(t), pre);
         }
-    } else {                          // (16 RB) x 16-unit tiles, K split over the waves
+    } else if constexpr (BF16W) {
+        const int NU = d.H / KW_TU;
+        if (M > 128 * max(1, 256 / NU)) {   // (16 RB) x 64-unit tiles
+            const int NR = kq_row_tiles(d, M);
+            const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
+            const int ntiles = NR * (d.H / KQ_TU);
+            for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+                switch (RB) {
+                    case 1: gru_kq_bf16<1>(d, R, layer, M, smem, t, NR); break;
+                    case 2: gru_kq_bf16<2>(d, R, layer, M, smem, t, NR); break;
+                    case 3: gru_kq_bf16<3>(d, R, layer, M, smem, t, NR); break;
+                    case 4: gru_kq_bf16<4>(d, R, layer, M, smem, t, NR); break;
+                    case 5: gru_kq_bf16<5>(d, R, layer, M, smem, t, NR); break;
+                    case 6: gru_kq_bf16<6>(d, R, layer, M, smem, t, NR); break;
+                    case 7: gru_kq_bf16<7>(d, R, layer, M, smem, t, NR); break;
+                    default: gru_kq_bf16<8>(d, R, layer, M, smem, t, NR); break;
+                }
+            }
+            return;
+        }
+        // (16 RB) x 32-unit tiles, K split over the waves
+        const int NR = kw_row_tiles(d, M);
+        const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
+        const int ntiles = NR * (d.H / KW_TU);
+        for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+            switch (RB) {
+                case 1: gru_kw_bf16<1>(d, R, layer, M, smem, t, NR); break;
+                case 2: gru_kw_bf16<2>(d, R, layer, M, smem, t, NR); break;
+                case 3: gru_kw_bf16<3>(d, R, layer, M, smem, t, NR); break;
+                case 4: gru_kw_bf16<4>(d, R, layer, M, smem, t, NR); break;
+                case 5: gru_kw_bf16<5>(d, R, layer, M, smem, t, NR); break;
+                case 6: gru_kw_bf16<6>(d, R, layer, M, smem, t, NR); break;
+                case 7: gru_kw_bf16<7>(d, R, layer, M, smem, t, NR); break;
+                default: gru_kw_bf16<8>(d, R, layer, M, smem, t, NR); break;
+            }
+        }
+    } else {                          // fp32: (16 RB) x 16-unit tiles, K split over the waves
         const int NR = ks_row_tiles(d, M);
         const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
         const int ntiles = NR * (d.H / KS_TU);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
             switch (RB) {
-                case 1: gru_ks<BF16W, 1>(d, R, layer, M, smem, t, NR); break;
-                case 2: gru_ks<BF16W, 2>(d, R, layer, M, smem, t, NR); break;
-                case 3: gru_ks<BF16W, 3>(d, R, layer, M, smem, t, NR); break;
-                case 4: gru_ks<BF16W, 4>(d, R, layer, M, smem, t, NR); break;
-                case 5: gru_ks<BF16W, 5>(d, R, layer, M, smem, t, NR); break;
-                case 6: gru_ks<BF16W, 6>(d, R, layer, M, smem, t, NR); break;
-                case 7: gru_ks<BF16W, 7>(d, R, layer, M, smem, t, NR); break;
-                default: gru_ks<BF16W, 8>(d, R, layer, M, smem, t, NR); break;
+                case 1: gru_ks_f32<1>(d, R, layer, M, smem, t, NR); break;
+                case 2: gru_ks_f32<2>(d, R, layer, M, smem, t, NR); break;
+                case 3: gru_ks_f32<3>(d, R, layer, M, smem, t, NR); break;
+                case 4: gru_ks_f32<4>(d, R, layer, M, smem, t, NR); break;
+                case 5: gru_ks_f32<5>(d, R, layer, M, smem, t, NR); break;
+                case 6: gru_ks_f32<6>(d, R, layer, M, smem, t, NR); break;
+                case 7: gru_ks_f32<7>(d, R, layer, M, smem, t, NR); break;
+                default: gru_ks_f32<8>(d, R, layer, M, smem, t, NR); break;
             }
         }
     }

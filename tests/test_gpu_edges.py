@@ -175,13 +175,15 @@ def test_host_rejects_oversized_frames():
     assert e.value.code == R.EINVAL
 
 
-@pytest.mark.parametrize("L,wd,E,H", [(1, F32, 128, 256), (2, F32, 128, 256), (1, 1, 128, 256), (2, 1, 192, 320)])
+@pytest.mark.parametrize("L,wd,E,H", [(1, F32, 128, 256), (2, F32, 128, 256), (1, 1, 128, 256), (2, 1, 192, 320),
+                                       (2, 1, 64, 128), (2, F32, 64, 128)])
 def test_gru_paths_by_row_count(L, wd, E, H):
     """Row counts on each side of the narrow path (<= 32 rows) and across the
-    tiled path's row-tile heights, all new keys, against the oracle. The last case has a
-    hidden size whose 16-unit tiles (20) do not split evenly over the 8 XCDs,
-    and input sizes (192, then 320) that are not multiples of 128, so that
-    bf16 K steps straddle the input / history boundary and reach past K."""
+    tiled path's row-tile heights, all new keys, against the oracle. H = 320
+    gives unit tiles (20 fp32 tiles of 16 units, 10 bf16 tiles of 32) that do
+    not split evenly over the 8 XCDs, with input sizes (192, then 320) that
+    are not multiples of 128; E = 64 gives a first layer whose input part is
+    a single K step."""
     m = ModelCfg(V=3000, E=E, H=H, L=L, wdtype=wd, maxent_log2=12, maxent_order=4)
     rng = np.random.default_rng(10 + L + 3 * wd)
     w = weights(m, rng, scale=0.08)

@@ -3,7 +3,8 @@
 A warm Large run has few new history keys per frame (Sec. 3: the history
 cache absorbs the rest), so most frames run the narrow path (at most 32
 rows) and the others the tiled path, whose row tiles shrink with the row
-count.
+count; bf16 tiles are 32 hidden units wide, and 64 wide once the 32-unit
+tiles would need more than one per CU (above 1024 rows at H = 1024).
 Here each path runs at E = 512, H = 1024: one fp32 layer (K = 1536), and two
 bf16 layers (K = 1536, then 2048). A first frame puts some keys in the
 history cache; the frame under test then has exactly M new history keys,
@@ -30,26 +31,29 @@ MODELS = {
     "bf16": ModelCfg(V=V, E=512, H=1024, L=2, wdtype=BF16, maxent_log2=16, maxent_order=4),
 }
 ROWS = (1, 15, 16, 17, 32, 33, 100, 256, 257)
+ROWS_BF16_WIDE = (1025, 1600)   # 64-unit bf16 tiles
 N_WARM = 24      # keys of the first frame
 N_CACHED = 8     # first-frame histories repeated in the frame under test
 KEYS = ("h_hash", "h_status", "h_rep", "q_status", "q_rep")
 
 
-def path_of(M, one):
+def path_of(name, M, one):
     if M <= 16 and one:
         return "narrow_preloaded"
     if M <= 32:
         return "narrow"
+    if name == "bf16":
+        return "tiled64" if M > 1024 else "tiled32"
     return "tiled"
 
 
 def cases():
     for name in MODELS:
-        for M in ROWS:
+        for M in ROWS + (ROWS_BF16_WIDE if name == "bf16" else ()):
             for sessions in (1, 2):
                 # two sessions split the rows: session 0 has M - M // 3, session 1 has M // 3
                 yield pytest.param(name, M, sessions,
-                                   id="%s-%s-M%d-s%d" % (name, path_of(M, sessions == 1), M, sessions))
+                                   id="%s-%s-M%d-s%d" % (name, path_of(name, M, sessions == 1), M, sessions))
 
 
 _W = {}
@@ -130,7 +134,7 @@ def test_gru_path_at_large_dims(name, M, sessions):
     w = weights(name)
     rng = np.random.default_rng(M * 7 + sessions)
     split = [M] if sessions == 1 else [M - M // 3, M // 3]
-    kw = dict(max_hist=512, max_query=2048, cap_hist=1 << 12, cap_query=1 << 14)
+    kw = dict(max_hist=2048, max_query=4096, cap_hist=1 << 12, cap_query=1 << 14)
     g = R.Scorer(m, w, Q_SIGN, 0, sessions=sessions, **kw)
     orc = [Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, w, Q_SIGN, 0,
                   cap_hist=kw["cap_hist"], cap_query=kw["cap_query"], seed=R.DEFAULT_SEED)
@@ -147,7 +151,7 @@ def test_gru_path_at_large_dims(name, M, sessions):
         assert res.gru_rows == N_WARM
         compare(outs[k], res, warm[k], m.wdtype == BF16, "%s warm s%d" % (name, k))
     frames = [frame_under_test(rng, m, warm[k], split[k]) for k in range(sessions)]
-    log("  %s M=%d sessions=%d: frame under test, path %s" % (name, M, sessions, path_of(M, sessions == 1)))
+    log("  %s M=%d sessions=%d: frame under test, path %s" % (name, M, sessions, path_of(name, M, sessions == 1)))
     if sessions == 1:
         outs = [g.score_frame(*to_dev(frames[0]))]
     else:
