@@ -690,6 +690,227 @@ __device__ __forceinline__ T *row_ptr(const Rows &R, T *arr, int m, size_t strid
     return shift_ptr(arr, o) + (size_t)(m - base) * stride;
 }
 
+// Many rows (more than one 16-unit tile per CU): fp32 tiles of 16 RB rows x
+// 64 hidden units (192 weight rows), 32-k steps (128 bytes per operand row;
+// E and H are multiples of 64, so a step lies wholly in one part). Wave
+// w = 4 g + uq takes row blocks g, g + 2, ... and units 16 uq .. + 15 over the
+// whole step: per row block and gate, two float4 fragments of 16 k, four
+// 16x16x4 MFMAs each, and no partial sums to exchange. Each step carries
+// twice the MFMA work of a 16-unit tile's step, with a quarter of the tiles
+// (12-13% faster at 2048-16384 rows; at most 512 rows, where 16-unit tiles
+// make one per CU, 64-unit tiles would leave each wave a single row block).
+constexpr int KF_TU = 64;                                  // hidden units per tile
+constexpr int KF_BROWS = 3 * KF_TU;                        // weight rows per tile
+constexpr int KF_BK = 32;                                  // K step (floats)
+constexpr int KF_LDA = 40;                                 // LDS row (floats): 128 bytes of operands, 32 of padding
+constexpr int KF_ROWS = 16 * KS_RBMAX + KF_BROWS;
+constexpr int KF_OPER = 2 * KF_ROWS * KF_LDA;              // two operand buffers (floats)
+constexpr int KF_PTRS = KF_OPER;                           // per tile row: destination, history source, input source
+constexpr int KF_HPREV = KF_PTRS + 16 * KS_RBMAX * 6;      // per tile row: h of the tile's 64 units
+static_assert(KF_HPREV + 16 * KS_RBMAX * KF_TU <= G_LDS_FLOATS, "64-unit fp32 tiles exceed the LDS buffer");
+
+typedef float (*KfLds)[KF_ROWS][KF_LDA];
+
+__device__ __forceinline__ int kf_row_tiles(const Dev &d, int M) {
+    const int NU = d.H / KF_TU;
+    const int R0 = max(1, 256 / NU);
+    return R0 * ((M + 128 * R0 - 1) / (128 * R0));
+}
+
+// A thread's share of one K step: 16-byte chunk t % 8 of A rows t / 8 and
+// t / 8 + 64 and of weight rows t / 8, t / 8 + 64, t / 8 + 128 (gate 0, 1, 2
+// of unit t / 8).
+struct KfStage {
+    float4 a0, a1, b0, b1, b2;
+};
+
+template <int RB>
+__device__ __forceinline__ void kf_load(KfStage &S, const u64 *ptrs, int a_r, int a_c4, int k0, int Kx,
+                                        const float *bp, size_t bstride) {
+    constexpr int BM = 16 * RB;
+    const bool xp = k0 < Kx;   // uniform
+    const int ko = (xp ? k0 : k0 - Kx) + a_c4;
+    const int r0 = min(a_r, BM - 1), r1 = min(a_r + 64, BM - 1);
+    S.a0 = ldg<float4>(reinterpret_cast<const float *>(ptrs[3 * r0 + (xp ? 2 : 1)]) + ko);
+    S.a1 = ldg<float4>(reinterpret_cast<const float *>(ptrs[3 * r1 + (xp ? 2 : 1)]) + ko);
+    S.b0 = ldg<float4>(bp + k0);
+    S.b1 = ldg<float4>(bp + bstride + k0);
+    S.b2 = ldg<float4>(bp + 2 * bstride + k0);
+}
+
+template <int RB>
+__device__ __forceinline__ void kf_store(const KfStage &S, KfLds As, int buf, int a_r, int a_c4) {
+    constexpr int BM = 16 * RB;
+    if (a_r < BM) *reinterpret_cast<float4 *>(&As[buf][a_r][a_c4]) = S.a0;
+    if (a_r + 64 < BM) *reinterpret_cast<float4 *>(&As[buf][a_r + 64][a_c4]) = S.a1;
+    *reinterpret_cast<float4 *>(&As[buf][BM + a_r][a_c4]) = S.b0;
+    *reinterpret_cast<float4 *>(&As[buf][BM + 64 + a_r][a_c4]) = S.b1;
+    *reinterpret_cast<float4 *>(&As[buf][BM + 128 + a_r][a_c4]) = S.b2;
+}
+
+// One K step of a wave of row group G and unit quarter uq. mid() runs after
+// the first row block's MFMAs (before them with one row block).
+template <int RB, int G, int NG, class MID>
+__device__ __forceinline__ void kf_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KfLds As,
+                                        int buf, int rl, int kc, int uq, MID mid) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    if constexpr (NRB == 0) {
+        mid();
+        return;
+    }
+    // the step's two 16-k halves one after the other: seven fragments live at a time
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        float4 b[3], a[NRB > 0 ? NRB : 1];
+#pragma unroll
+        for (int q = 0; q < 3; ++q)
+            b[q] = *reinterpret_cast<const float4 *>(&As[buf][16 * RB + 64 * q + 16 * uq + rl][kc + 16 * h]);
+#pragma unroll
+        for (int i = 0; i < NRB; ++i) a[i] = *reinterpret_cast<const float4 *>(&As[buf][16 * (G + 2 * i) + rl][kc + 16 * h]);
+#pragma unroll
+        for (int i = 0; i < NRB; ++i) {
+            if (h == 0 && (i == 1 || NRB == 1)) mid();
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[0][c], acc[i][0], 0, 0, 0);
+                acc[i][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[1][c], acc[i][1], 0, 0, 0);
+                acc[i][NG] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[2][c], acc[i][NG], 0, 0, 0);
+            }
+        }
+    }
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void kf_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4],
+                                         const KsEpi &ep, int uq, int lane) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    const int eu = lane & 15;
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+        // D[row][col] sits in lane 16 * (row / 4) + col, element row % 4
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = 16 * (G + 2 * i) + 4 * (lane >> 4) + e;
+            const u64 dp = ep.ptrs[3 * row];
+            if (dp) {
+                const float rr = sigmoidf_(acc[i][0][e] + ep.br);
+                const float z = sigmoidf_(acc[i][1][e] + ep.bz);
+                const float n = tanhf(acc[i][2][e] + ep.bn + rr * acc[i][3][e]);
+                const float hn = (1.0f - z) * n + z * ep.hprev[row * KF_TU + 16 * uq + eu];
+                reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+            }
+        }
+    }
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void kf_waves(KfLds As, const KsEpi &ep, int a_r, int a_c4, int Kx, int K, const float *bp,
+                                         size_t bstride, int w, int lane) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    f4_t acc[NRB > 0 ? NRB : 1][4];   // [row block G + 2 i][reset, update, candidate input part, history part]
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = f4_t{0, 0, 0, 0};
+    const int uq = w & 3;
+    const int rl = lane & 15, kc = 4 * (lane >> 4);
+    const int nk = K / KF_BK, nx = Kx / KF_BK;   // nx >= 2
+    KfStage S0, S1;
+    kf_load<RB>(S0, ep.ptrs, a_r, a_c4, KF_BK, Kx, bp, bstride);
+    kf_load<RB>(S1, ep.ptrs, a_r, a_c4, 2 * KF_BK, Kx, bp, bstride);
+    auto step = [&](int kt, auto NGc, auto PARc) {
+        constexpr int NG = decltype(NGc)::value, PAR = decltype(PARc)::value;
+        KfStage &St = PAR == 0 ? S0 : S1;
+        kf_step<RB, G, NG>(acc, As, PAR, rl, kc, uq, [&] {
+            if (kt + 1 < nk) kf_store<RB>(St, As, 1 - PAR, a_r, a_c4);
+        });
+        // past the last step the stage re-reads the last step (unused)
+        kf_load<RB>(St, ep.ptrs, a_r, a_c4, min(kt + 3, nk - 1) * KF_BK, Kx, bp, bstride);
+        __syncthreads();
+    };
+    using X = std::integral_constant<int, 2>;
+    using Hh = std::integral_constant<int, 3>;
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    int kt = 0;
+    for (; kt + 1 < nx; kt += 2) {
+        step(kt, X(), P0());
+        step(kt + 1, X(), P1());
+    }
+    if (kt < nx) step(kt++, X(), P0());
+    if (kt & 1) step(kt++, Hh(), P1());
+    for (; kt + 1 < nk; kt += 2) {
+        step(kt, Hh(), P0());
+        step(kt + 1, Hh(), P1());
+    }
+    if (kt < nk) step(kt, Hh(), P0());
+    kf_gates<RB, G>(acc, ep, uq, lane);
+}
+
+template <int RB>
+__device__ __forceinline__ void gru_kf_f32(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
+                                           int NR) {
+    constexpr int BM = 16 * RB;
+    const int NU = d.H / KF_TU;
+    int rt, ut;
+    if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles
+        const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
+        rt = idx / per;
+        ut = xcd + 8 * (idx % per);
+    } else {
+        rt = tile / NU;
+        ut = tile % NU;
+    }
+    const int m0 = rt * BM, j0 = ut * KF_TU;
+    if (rt >= NR || m0 >= M) return;   // block-uniform
+
+    KfLds As = reinterpret_cast<KfLds>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KF_PTRS);   // [BM][3]
+    float *hprev = smem + KF_HPREV;                         // [BM][64]
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H;
+    const int K = Kx + d.H;
+    const float *Wp = reinterpret_cast<const float *>(d.Wl);
+    // the tile's row pointers, as for the 16-unit tiles
+    if (tid < BM) {
+        const int m = min(m0 + tid, M - 1);
+        const RowSrc src = row_source(d, R, layer, m, M);
+        ptrs[3 * tid] = m0 + tid < M ? (u64)row_at(R, d.f_rowdst, m) : 0;
+        ptrs[3 * tid + 1] = (u64)src.h;
+        ptrs[3 * tid + 2] = (u64)src.x;
+    }
+    __syncthreads();
+    // loaders: rows tid / 8 (+ 64), chunk tid % 8 of 4 floats; weight rows
+    // j0 + tid / 8 of each gate
+    const int a_r = tid >> 3, a_c4 = (tid & 7) * 4;
+    const float *bp = Wp + (size_t)(j0 + a_r) * K + a_c4;
+    const size_t bstride = (size_t)d.H * K;
+    // step 0 into LDS, with the epilogue's h: thread (row tid / 64 + 8 p, unit tid % 64)
+    const int hi = tid >> 6, hu = tid & 63;
+    float hv[2 * RB];
+#pragma unroll
+    for (int p = 0; p < 2 * RB; ++p) hv[p] = reinterpret_cast<const float *>(ptrs[3 * (hi + 8 * p) + 1])[j0 + hu];
+    KsEpi ep;
+    ep.ptrs = ptrs;
+    ep.hprev = hprev;
+    ep.j = j0 + 16 * (w & 3) + (lane & 15);
+    ep.br = d.bl[ep.j];
+    ep.bz = d.bl[d.H + ep.j];
+    ep.bn = d.bl[2 * d.H + ep.j];
+    ep.lofs = (size_t)layer * d.H;
+    {
+        KfStage S;
+        kf_load<RB>(S, ptrs, a_r, a_c4, 0, Kx, bp, bstride);
+        kf_store<RB>(S, As, 0, a_r, a_c4);
+    }
+#pragma unroll
+    for (int p = 0; p < 2 * RB; ++p) hprev[(hi + 8 * p) * KF_TU + hu] = hv[p];
+    __syncthreads();
+    if (w < 4) kf_waves<RB, 0>(As, ep, a_r, a_c4, Kx, K, bp, bstride, w, lane);
+    else kf_waves<RB, 1>(As, ep, a_r, a_c4, Kx, K, bp, bstride, w, lane);
+    __syncthreads();   // LDS is reused by the next tile
+}
+
 // -------------------- tiled path (more than 32 rows): bf16 ------------------
 // 16 RB rows x 32 hidden units (96 weight rows) per tile, 64-k steps (128
 // bytes per operand row), double-buffered LDS and two register stages as in
@@ -1262,7 +1483,26 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
                 default: gru_kw_bf16<8>(d, R, layer, M, smem, t, NR); break;
             }
         }
-    } else {                          // fp32: (16 RB) x 16-unit tiles, K split over the waves
+    } else {
+        if (M > 128 * max(1, 256 / (d.H / KS_TU))) {   // fp32: (16 RB) x 64-unit tiles
+            const int NR = kf_row_tiles(d, M);
+            const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
+            const int ntiles = NR * (d.H / KF_TU);
+            for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+                switch (RB) {
+                    case 1: gru_kf_f32<1>(d, R, layer, M, smem, t, NR); break;
+                    case 2: gru_kf_f32<2>(d, R, layer, M, smem, t, NR); break;
+                    case 3: gru_kf_f32<3>(d, R, layer, M, smem, t, NR); break;
+                    case 4: gru_kf_f32<4>(d, R, layer, M, smem, t, NR); break;
+                    case 5: gru_kf_f32<5>(d, R, layer, M, smem, t, NR); break;
+                    case 6: gru_kf_f32<6>(d, R, layer, M, smem, t, NR); break;
+                    case 7: gru_kf_f32<7>(d, R, layer, M, smem, t, NR); break;
+                    default: gru_kf_f32<8>(d, R, layer, M, smem, t, NR); break;
+                }
+            }
+            return;
+        }
+        // fp32: (16 RB) x 16-unit tiles, K split over the waves
         const int NR = ks_row_tiles(d, M);
         const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
         const int ntiles = NR * (d.H / KS_TU);

@@ -3,8 +3,9 @@
 A warm Large run has few new history keys per frame (Sec. 3: the history
 cache absorbs the rest), so most frames run the narrow path (at most 32
 rows) and the others the tiled path, whose row tiles shrink with the row
-count; bf16 tiles are 32 hidden units wide, and 64 wide once the 32-unit
-tiles would need more than one per CU (above 1024 rows at H = 1024).
+count. fp32 tiles are 16 hidden units wide, and 64 wide once the 16-unit
+tiles would need more than one per CU (above 512 rows at H = 1024); bf16
+tiles are 32 wide, and 64 wide above 1024 rows.
 Here each path runs at E = 512, H = 1024: one fp32 layer (K = 1536), and two
 bf16 layers (K = 1536, then 2048). A first frame puts some keys in the
 history cache; the frame under test then has exactly M new history keys,
@@ -31,7 +32,7 @@ MODELS = {
     "bf16": ModelCfg(V=V, E=512, H=1024, L=2, wdtype=BF16, maxent_log2=16, maxent_order=4),
 }
 ROWS = (1, 15, 16, 17, 32, 33, 100, 256, 257)
-ROWS_BF16_WIDE = (1025, 1600)   # 64-unit bf16 tiles
+ROWS_WIDE = {"fp32": (513, 1100), "bf16": (1025, 1600)}   # 64-unit tiles
 N_WARM = 24      # keys of the first frame
 N_CACHED = 8     # first-frame histories repeated in the frame under test
 KEYS = ("h_hash", "h_status", "h_rep", "q_status", "q_rep")
@@ -44,12 +45,12 @@ def path_of(name, M, one):
         return "narrow"
     if name == "bf16":
         return "tiled64" if M > 1024 else "tiled32"
-    return "tiled"
+    return "tiled64" if M > 512 else "tiled16"
 
 
 def cases():
     for name in MODELS:
-        for M in ROWS + (ROWS_BF16_WIDE if name == "bf16" else ()):
+        for M in ROWS + ROWS_WIDE[name]:
             for sessions in (1, 2):
                 # two sessions split the rows: session 0 has M - M // 3, session 1 has M // 3
                 yield pytest.param(name, M, sessions,
