@@ -443,10 +443,12 @@ __device__ __forceinline__ void ks_store(const KsStage<(16 * RB + 31) / 32> &S, 
 // One K step of a wave of row group G: its row blocks G, G + 2, ... x
 // (reset, update, candidate) over its 16 k of the step, four per MFMA. NG:
 // the candidate gate's accumulator (2: input part, 3: history part). mid()
-// runs after the first k's MFMAs: the caller stores the next step's operands
-// into the other LDS buffer there, so that the stores drain while the step's
-// remaining MFMAs run rather than between its last MFMA and the barrier
-// (6-8% faster loops than storing after the MFMAs).
+// is where the caller stores the next step's operands into the other LDS
+// buffer: after the first k's MFMAs for row group 0, before any MFMA for row
+// group 1, so that the stores of the two waves sharing a SIMD drain while the
+// other wave's MFMAs run, rather than all between the last MFMA and the
+// barrier (6-8% faster loops than storing after the MFMAs, and another 2-3%
+// from staggering the two groups).
 template <int RB, int G, int NG, class MID>
 __device__ __forceinline__ void ks_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KsLds As, int buf,
                                         int rl, int kc, MID mid) {
@@ -462,7 +464,7 @@ __device__ __forceinline__ void ks_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB -
     for (int i = 0; i < NRB; ++i) a[i] = *reinterpret_cast<const float4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        if (c == 1) mid();
+        if (c == (G == 0 ? 1 : 0)) mid();
 #pragma unroll
         for (int i = 0; i < NRB; ++i) {
             acc[i][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][c], b[0][c], acc[i][0], 0, 0, 0);
