@@ -490,8 +490,10 @@ struct KsEpi {
 // quarter][part][lane], over the operand buffers; wave q then finishes its
 // group's block q (when it has one): the four quarters' partials are added
 // in quarter order (the same fixed order whichever wave finishes), and each
-// lane applies the gates to its four rows of one unit.
-template <int RB, int G>
+// lane applies the gates to its four rows of one unit. NP: u64 pointers per
+// tile row (the destination first; with 5, the fifth is where the bf16 copy
+// of h' goes for the next layer, or 0).
+template <int RB, int G, int NP>
 __device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], float *smem,
                                          const KsEpi &ep, int w, int lane, int tid) {
     constexpr int NRB = (RB - G + 1) / 2;
@@ -533,13 +535,17 @@ __device__ __forceinline__ void ks_gates(const f4_t (&acc)[(RB - G + 1) / 2 > 0 
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int row = 16 * (G + 2 * q) + 4 * (lane >> 4) + e;
-        const u64 dp = ep.ptrs[3 * row];
+        const u64 dp = ep.ptrs[NP * row];
         if (dp) {
             const float rr = sigmoidf_(sum[0][e] + ep.br);
             const float z = sigmoidf_(sum[1][e] + ep.bz);
             const float n = tanhf(sum[2][e] + ep.bn + rr * sum[3][e]);
             const float hn = (1.0f - z) * n + z * ep.hprev[row * KS_TU + eu];
             reinterpret_cast<float *>(dp)[ep.lofs + ep.j] = hn;
+            if constexpr (NP == 5) {
+                const u64 xp = ep.ptrs[NP * row + 4];
+                if (xp) reinterpret_cast<uint16_t *>(xp)[ep.j] = f32_to_bf16(hn);
+            }
         }
     }
 }
@@ -598,7 +604,7 @@ __device__ __forceinline__ void ks_waves(KsLds As, float *smem, const KsEpi &ep,
         step(kt + 1, Hh(), P1());
     }
     if (kt < nk) step(kt, Hh(), P0());
-    ks_gates<RB, G>(acc, smem, ep, w, lane, tid);
+    ks_gates<RB, G, 3>(acc, smem, ep, w, lane, tid);
 }
 
 template <int RB>
@@ -913,7 +919,221 @@ __device__ __forceinline__ void gru_kf_f32(const Dev &d, const Rows &R, int laye
     __syncthreads();   // LDS is reused by the next tile
 }
 
-// -------------------- tiled path (more than 32 rows): bf16 ------------------
+// ---------------- tiled path (33 rows and more): bf16, 16-unit tiles --------
+// For few rows (while 32-unit tiles would be at most two row blocks high:
+// here a step of 128 k carries twice the MFMA work of a 32-unit tile's 64-k
+// step at the same height, 1-8 us faster per launch at 33-256 rows). The fp32
+// tile's shape and schedule (16 RB rows x 16 hidden units, 8 waves as
+// 2 row groups x 4 K quarters, double-buffered LDS, loads three steps ahead)
+// with bf16 operands: the history rows were rounded once per frame by the
+// keys kernel, and the second layer's input is the bf16 copy of the first
+// layer's h' that its tiles' epilogue writes. A step is 128 k, i.e. the same
+// 256 bytes per operand row as an fp32 step, so the LDS layout and every LDS
+// address are the fp32 tile's; a wave's quarter is 32 k, one 16 x 16 x 32 MFMA
+// per row block and gate part. A step may straddle the input / history
+// boundary or reach past K (E and H are multiples of 64): each 8-k chunk is
+// loaded from its own part (clamped inside K), and a wave's quarter, which
+// lies wholly in one part (or past K), feeds zeros to the candidate gate's
+// other accumulator (or to every product).
+constexpr int KSB_BK = 128;                               // K step (bf16 elements)
+constexpr int KSB_PTRS = KS_OPER;                         // per tile row: dst, h fp32, h bf16, x bf16, x copy dst
+constexpr int KSB_HPREV = KSB_PTRS + 16 * KS_RBMAX * 10;  // per tile row: h of the tile's 16 units
+static_assert(KSB_HPREV + 16 * KS_RBMAX * KS_TU <= G_LDS_FLOATS, "bf16 tiles exceed the LDS buffer");
+
+template <int NPA>
+struct KsbStage {
+    uint4 a[NPA], b0, b1;
+};
+
+// Every thread issues the same loads, none behind a branch: a chunk past K
+// re-reads the last chunk inside K (its products are zeroed), rows past the
+// tile re-read its last row. bp0, bp1: the starts of the thread's weight rows.
+template <int RB>
+__device__ __forceinline__ void ksb_load(KsbStage<(16 * RB + 31) / 32> &S, const u64 *ptrs, int a_r, int a_k, int k0,
+                                         int Kx, int K, const uint16_t *bp0, const uint16_t *bp1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+    const int k = min(k0 + a_k, K - 8);
+    const bool xp = k < Kx;
+#pragma unroll
+    for (int p = 0; p < NPA; ++p) {
+        const int row = min(a_r + 32 * p, BM - 1);
+        const uint16_t *src = reinterpret_cast<const uint16_t *>(ptrs[5 * row + (xp ? 3 : 2)]);
+        S.a[p] = ldg<uint4>(src + (xp ? k : k - Kx));
+    }
+    S.b0 = ldg<uint4>(bp0 + k);
+    S.b1 = ldg<uint4>(bp1 + k);
+}
+
+template <int RB>
+__device__ __forceinline__ void ksb_store(const KsbStage<(16 * RB + 31) / 32> &S, KsLds As, int buf, int a_r, int a_c,
+                                          bool has_b1) {
+    constexpr int BM = 16 * RB, NPA = (BM + 31) / 32;
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (a_r + 32 * p < BM) *reinterpret_cast<uint4 *>(&As[buf][a_r + 32 * p][a_c]) = S.a[p];
+    *reinterpret_cast<uint4 *>(&As[buf][BM + a_r][a_c]) = S.b0;
+    if (has_b1) *reinterpret_cast<uint4 *>(&As[buf][BM + 32 + a_r][a_c]) = S.b1;
+}
+
+// One K step of a wave of row group G: its row blocks G, G + 2, ... x
+// (reset, update, candidate input part, candidate history part) over its 32 k
+// of the step. live: the quarter lies inside K; xp: in the input part. mid()
+// runs after the first row block's MFMAs (before them with one row block), as
+// in the fp32 step.
+template <int RB, int G, class MID>
+__device__ __forceinline__ void ksb_step(f4_t (&acc)[(RB - G + 1) / 2 > 0 ? (RB - G + 1) / 2 : 1][4], KsLds As,
+                                         int buf, int rl, int kc, bool live, bool xp, MID mid) {
+    constexpr int NRB = (RB - G + 1) / 2;
+    if constexpr (NRB == 0) {
+        mid();
+        return;
+    }
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    uint4 g[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) g[q] = *reinterpret_cast<const uint4 *>(&As[buf][16 * RB + 16 * q + rl][kc]);
+    bf8_t b[4];
+    b[0] = __builtin_bit_cast(bf8_t, g[0]);
+    b[1] = __builtin_bit_cast(bf8_t, g[1]);
+    b[2] = __builtin_bit_cast(bf8_t, xp ? g[2] : z);
+    b[3] = __builtin_bit_cast(bf8_t, xp ? z : g[2]);
+    bf8_t a[NRB > 0 ? NRB : 1];
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(&As[buf][16 * (G + 2 * i) + rl][kc]);
+        a[i] = __builtin_bit_cast(bf8_t, live ? v : z);
+    }
+#pragma unroll
+    for (int i = 0; i < NRB; ++i) {
+        if (i == 1 || (NRB == 1 && i == 0)) mid();
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[q], acc[i][q], 0, 0, 0);
+    }
+}
+
+template <int RB, int G>
+__device__ __forceinline__ void ksb_waves(KsLds As, float *smem, const KsEpi &ep, int a_r, int a_k, int a_c, int Kx,
+                                          int K, const uint16_t *bp0, const uint16_t *bp1, bool has_b1, int w,
+                                          int lane, int tid) {
+    constexpr int NPA = (16 * RB + 31) / 32;
+    constexpr int NRB = (RB - G + 1) / 2;
+    f4_t acc[NRB > 0 ? NRB : 1][4];   // [row block G + 2 i][reset, update, candidate input part, history part]
+#pragma unroll
+    for (int i = 0; i < NRB; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[i][q] = f4_t{0, 0, 0, 0};
+    const int rl = lane & 15, kc = 16 * (w & 3) + 4 * (lane >> 4);   // kc in floats: bf16 k = 32 (w % 4) + 8 (lane / 16)
+    const int ns = (K + KSB_BK - 1) / KSB_BK;                         // >= 1
+    // two register stages as in the fp32 tile: S0 carries the odd steps and
+    // S1 the even ones from step 2 on; LDS buffer s & 1 holds step s
+    KsbStage<NPA> S0, S1;
+    ksb_load<RB>(S0, ep.ptrs, a_r, a_k, min(1, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+    ksb_load<RB>(S1, ep.ptrs, a_r, a_k, min(2, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+    auto step = [&](int st, auto PARc) {
+        constexpr int PAR = decltype(PARc)::value;
+        const int kq = st * KSB_BK + 32 * (w & 3);   // wave-uniform
+        KsbStage<NPA> &St = PAR == 0 ? S0 : S1;
+        ksb_step<RB, G>(acc, As, PAR, rl, kc, kq < K, kq < Kx, [&] {
+            if (st + 1 < ns) ksb_store<RB>(St, As, 1 - PAR, a_r, a_c, has_b1);
+        });
+        // past the last step the stage re-reads the last step (unused), so
+        // that every step issues the same loads and the waits stay exact
+        ksb_load<RB>(St, ep.ptrs, a_r, a_k, min(st + 3, ns - 1) * KSB_BK, Kx, K, bp0, bp1);
+        __syncthreads();
+    };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    int st = 0;
+    for (; st + 1 < ns; st += 2) {
+        step(st, P0());
+        step(st + 1, P1());
+    }
+    if (st < ns) step(st, P0());
+    ks_gates<RB, G, 5>(acc, smem, ep, w, lane, tid);
+}
+
+template <int RB>
+__device__ __forceinline__ void gru_ks_bf16(const Dev &d, const Rows &R, int layer, int M, float *smem, int tile,
+                                            int NR) {
+    constexpr int BM = 16 * RB;
+    constexpr int NPA = (BM + 31) / 32;
+    const int NU = d.H / KS_TU;
+    int rt, ut;
+    if ((NU & 7) == 0) {   // every XCD keeps its own unit tiles (and their weights in its L2)
+        const int xcd = tile & 7, idx = tile >> 3, per = NU >> 3;
+        rt = idx / per;
+        ut = xcd + 8 * (idx % per);
+    } else {
+        rt = tile / NU;
+        ut = tile % NU;
+    }
+    const int m0 = rt * BM, j0 = ut * KS_TU;
+    if (rt >= NR || m0 >= M) return;   // block-uniform
+
+    KsLds As = reinterpret_cast<KsLds>(smem);
+    u64 *ptrs = reinterpret_cast<u64 *>(smem + KSB_PTRS);   // [BM][5]
+    float *hprev = smem + KSB_HPREV;                         // [BM][16]
+
+    const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+    const int Kx = layer == 0 ? d.E : d.H;
+    const int K = Kx + d.H;
+    const uint16_t *Wp = reinterpret_cast<const uint16_t *>(d.Wl);
+
+    // the tile's row pointers (rows past M read row M - 1: their products
+    // only reach rows the epilogue skips): destination, fp32 h (this layer's
+    // part), bf16 h (this layer's part), bf16 x (embedding row, or the bf16
+    // copy of the first layer's h'), and where the first layer's tiles put
+    // that copy when there is a second layer
+    if (tid < BM) {
+        const int m = min(m0 + tid, M - 1);
+        const bool live = m0 + tid < M;
+        ptrs[5 * tid] = live ? row_at(R, d.f_rowdst, m) : 0;
+        ptrs[5 * tid + 1] = row_at(R, d.f_rowh, m) + (u64)layer * d.H * 4;
+        ptrs[5 * tid + 2] = row_at(R, d.f_rowhb, m) + (u64)layer * d.H * 2;
+        ptrs[5 * tid + 3] = layer == 0 ? (u64)(reinterpret_cast<const uint16_t *>(d.emb) +
+                                               (size_t)(unsigned)row_at(R, d.f_roww, m) * d.E)
+                                       : (u64)row_ptr(R, d.f_xbf, m, d.H);
+        ptrs[5 * tid + 4] = live && layer == 0 && d.L == 2 ? (u64)row_ptr(R, d.f_xbf, m, d.H) : 0;
+    }
+    __syncthreads();
+    // A loader: rows tid/16 + 32 p, 8 consecutive k at 8 (tid % 16). B
+    // loader: weight rows tid/16 (and tid/16 + 32 for tid < 256): gate
+    // row / 16, unit row % 16. a_c: the chunk's LDS column in floats.
+    const int a_r = tid >> 4, a_k = (tid & 15) * 8, a_c = (tid & 15) * 4;
+    const uint16_t *bp0 = Wp + (size_t)((a_r >> 4) * d.H + j0 + (a_r & 15)) * K;   // row starts: the loads add k
+    const uint16_t *bp1 = Wp + (size_t)(2 * d.H + j0 + (a_r & 15)) * K;
+    const bool has_b1 = tid < 256;   // wave-uniform
+
+    // step 0 into LDS, with the epilogue's fp32 h (the tile's 16 units of each
+    // row's history): thread (row i, unit u) for rows i = tid/16 + 32 p
+    const int hi = tid >> 4, hu = tid & 15;
+    float hv[NPA];
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hv[p] = reinterpret_cast<const float *>(ptrs[5 * (hi + 32 * p) + 1])[j0 + hu];
+    KsEpi ep;
+    ep.ptrs = ptrs;
+    ep.hprev = hprev;
+    ep.j = j0 + hu;
+    ep.br = d.bl[ep.j];
+    ep.bz = d.bl[d.H + ep.j];
+    ep.bn = d.bl[2 * d.H + ep.j];
+    ep.lofs = (size_t)layer * d.H;
+    {
+        KsbStage<NPA> S;
+        ksb_load<RB>(S, ptrs, a_r, a_k, 0, Kx, K, bp0, bp1);
+        ksb_store<RB>(S, As, 0, a_r, a_c, has_b1);
+    }
+#pragma unroll
+    for (int p = 0; p < NPA; ++p)
+        if (hi + 32 * p < BM) hprev[(hi + 32 * p) * KS_TU + hu] = hv[p];
+    __syncthreads();
+    if (w < 4) ksb_waves<RB, 0>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
+    else ksb_waves<RB, 1>(As, smem, ep, a_r, a_k, a_c, Kx, K, bp0, bp1, has_b1, w, lane, tid);
+    __syncthreads();   // LDS is reused by the next tile
+}
+
+// --------------- tiled path (more rows): bf16, 32- and 64-unit tiles --------
 // 16 RB rows x 32 hidden units (96 weight rows) per tile, 64-k steps (128
 // bytes per operand row), double-buffered LDS and two register stages as in
 // the fp32 tile. E and H are multiples of 64, so a step lies wholly in the
@@ -1451,6 +1671,25 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
         }
     } else if constexpr (BF16W) {
         const int NU = d.H / KW_TU;
+        const int NRw = kw_row_tiles(d, M);
+        if ((M + 15) / 16 <= 2 * NRw) {   // 32-unit tiles would be 1 or 2 row blocks high: (16 RB) x 16-unit tiles
+            const int NR = ks_row_tiles(d, M);
+            const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
+            const int ntiles = NR * (d.H / KS_TU);
+            for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+                switch (RB) {
+                    case 1: gru_ks_bf16<1>(d, R, layer, M, smem, t, NR); break;
+                    case 2: gru_ks_bf16<2>(d, R, layer, M, smem, t, NR); break;
+                    case 3: gru_ks_bf16<3>(d, R, layer, M, smem, t, NR); break;
+                    case 4: gru_ks_bf16<4>(d, R, layer, M, smem, t, NR); break;
+                    case 5: gru_ks_bf16<5>(d, R, layer, M, smem, t, NR); break;
+                    case 6: gru_ks_bf16<6>(d, R, layer, M, smem, t, NR); break;
+                    case 7: gru_ks_bf16<7>(d, R, layer, M, smem, t, NR); break;
+                    default: gru_ks_bf16<8>(d, R, layer, M, smem, t, NR); break;
+                }
+            }
+            return;
+        }
         if (M > 128 * max(1, 256 / NU)) {   // (16 RB) x 64-unit tiles
             const int NR = kq_row_tiles(d, M);
             const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
@@ -1470,7 +1709,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gru(Dev d, SessList sl, int layer
             return;
         }
         // (16 RB) x 32-unit tiles, K split over the waves
-        const int NR = kw_row_tiles(d, M);
+        const int NR = NRw;
         const int RB = __builtin_amdgcn_readfirstlane(((M + 15) / 16 + NR - 1) / NR);
         const int ntiles = NR * (d.H / KW_TU);
         for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {

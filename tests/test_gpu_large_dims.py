@@ -5,7 +5,7 @@ cache absorbs the rest), so most frames run the narrow path (at most 32
 rows) and the others the tiled path, whose row tiles shrink with the row
 count. fp32 tiles are 16 hidden units wide, and 64 wide once the 16-unit
 tiles would need more than one per CU (above 512 rows at H = 1024); bf16
-tiles are 32 wide, and 64 wide above 1024 rows.
+tiles are 16 wide up to 256 rows, 32 wide up to 1024 and 64 wide above.
 Here each path runs at E = 512, H = 1024: one fp32 layer (K = 1536), and two
 bf16 layers (K = 1536, then 2048). A first frame puts some keys in the
 history cache; the frame under test then has exactly M new history keys,
@@ -44,7 +44,7 @@ def path_of(name, M, one):
     if M <= 32:
         return "narrow"
     if name == "bf16":
-        return "tiled64" if M > 1024 else "tiled32"
+        return "tiled64" if M > 1024 else "tiled32" if M > 256 else "tiled16"
     return "tiled64" if M > 512 else "tiled16"
 
 
