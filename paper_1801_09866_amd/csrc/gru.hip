@@ -920,10 +920,11 @@ __device__ __forceinline__ void gru_kf_f32(const Dev &d, const Rows &R, int laye
 }
 
 // ---------------- tiled path (33 rows and more): bf16, 16-unit tiles --------
-// For few rows (while 32-unit tiles would be at most two row blocks high:
-// here a step of 128 k carries twice the MFMA work of a 32-unit tile's 64-k
-// step at the same height, 1-8 us faster per launch at 33-256 rows). The fp32
-// tile's shape and schedule (16 RB rows x 16 hidden units, 8 waves as
+// For few rows, while 32-unit tiles would be at most two row blocks high
+// (at H = 1024, 256 rows): their eight row tiles per unit tile pad such row
+// counts to whole row blocks and take twice the K steps, and these tiles
+// measured 1-8 us faster per launch at 33-256 rows. The fp32 tile's shape
+// and schedule (16 RB rows x 16 hidden units, 8 waves as
 // 2 row groups x 4 K quarters, double-buffered LDS, loads three steps ahead)
 // with bf16 operands: the history rows were rounded once per frame by the
 // keys kernel, and the second layer's input is the bf16 copy of the first
