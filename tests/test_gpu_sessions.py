@@ -9,10 +9,10 @@ import numpy as np
 import pytest
 import torch
 
-from harness import ATOL, RTOL, close, log
+from harness import ATOL, BF16_ATOL, RTOL, close, log
 from oracle import Q_SIGDIG, Q_SIGN, Oracle
 from paper_1801_09866_amd import rnnlm as R
-from paper_1801_09866_amd.workload import F32, ModelCfg
+from paper_1801_09866_amd.workload import BF16, F32, ModelCfg
 
 pytestmark = pytest.mark.gpu
 
@@ -116,28 +116,36 @@ def test_a_device_error_in_one_session_is_sticky_for_the_context():
     assert g.stats()["device_error"] == 0
 
 
-def test_eight_sessions_of_maximal_frames():
+@pytest.mark.parametrize("wd", [F32, BF16], ids=["fp32", "bf16"])
+def test_eight_sessions_of_maximal_frames(wd):
     """The largest launch the API allows: 8 sessions, each frame at the
     planner's maxima (2048 histories, 8192 queries), with uniform targets and
     a second block that repeats half of each session's histories and many of
     its queries (cache hits). Every session must equal a context of its own,
-    and one session the oracle."""
+    and one session the oracle. At H = 128 the 8-session launches run the
+    64-unit tiles (fp32: both blocks, 16384 and 8192 GRU rows; bf16: the
+    first block) and the 32-unit bf16 tiles (the second block), while a
+    context of its own runs the 16-unit tiles on at most 2048 rows; bf16
+    results are compared at the bf16 tolerance, since the tiles' summation
+    orders differ."""
+    m = ModelCfg(V=M.V, E=M.E, H=M.H, L=M.L, wdtype=wd, maxent_log2=M.maxent_log2, maxent_order=M.maxent_order)
+    tol = (BF16_ATOL, 0.0) if wd == BF16 else (ATOL, RTOL)
     rng = np.random.default_rng(88)
-    w = weights(M, rng)
+    w = weights(m, rng)
     S, n_h, n_q = 8, 2048, 8192
     caps = (1 << 14, 1 << 16)
     kw = dict(max_hist=n_h, max_query=n_q, cap_hist=caps[0], cap_query=caps[1])
-    multi = R.Scorer(M, w, Q_SIGN, 0, sessions=S, **kw)
-    solo = R.Scorer(M, w, Q_SIGN, 0, **kw)
+    multi = R.Scorer(m, w, Q_SIGN, 0, sessions=S, **kw)
+    solo = R.Scorer(m, w, Q_SIGN, 0, **kw)
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
     blocks = []
     for t in range(2):
         frs = []
         for k in range(S):
-            vec = (np.tanh(rng.standard_normal((n_h, M.L * M.H))) * 0.9).astype(np.float32)
-            words = rng.integers(0, M.V, (n_h, 3)).astype(np.int32)
+            vec = (np.tanh(rng.standard_normal((n_h, m.L * m.H))) * 0.9).astype(np.float32)
+            words = rng.integers(0, m.V, (n_h, 3)).astype(np.int32)
             qh = rng.integers(0, n_h, n_q).astype(np.int32)
-            qt = rng.integers(0, M.V, n_q).astype(np.int32)
+            qt = rng.integers(0, m.V, n_q).astype(np.int32)
             if t == 1:   # the previous frame's first half of histories, and their queries, again
                 pv, pw, pqh, pqt = blocks[0][k]
                 vec[: n_h // 2], words[: n_h // 2] = pv[: n_h // 2], pw[: n_h // 2]
@@ -155,18 +163,18 @@ def test_eight_sessions_of_maximal_frames():
             for key in KEYS:
                 a, b = outs[k][key], o1[key]
                 if key in ("scores", "hnew"):
-                    assert close(a.cpu().numpy(), b.cpu().numpy(), ATOL, RTOL)[0], (t, k, key)
+                    assert close(a.cpu().numpy(), b.cpu().numpy(), *tol)[0], (t, k, key)
                 else:
                     assert torch.equal(a, b), (t, k, key)
             if t == 1:
                 assert (outs[k]["q_status"] == R.Q_SCORE_HIT).sum().item() > n_q // 4, k
     assert multi.stats()["device_error"] == 0
-    o = Oracle(M.V, M.E, M.H, M.L, M.maxent_log2, M.maxent_order, w, Q_SIGN, 0,
+    o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, w, Q_SIGN, 0,
                cap_hist=caps[0], cap_query=caps[1], seed=R.DEFAULT_SEED)
     o.score_frame(*blocks[0][3])
     res = o.score_frame(*blocks[1][3])
     for key, want in (("q_status", res.q_status), ("q_rep", res.q_rep), ("h_status", res.h_status),
                       ("h_rep", res.h_rep)):
         assert np.array_equal(outs[3][key].cpu().numpy(), want), key
-    assert close(outs[3]["scores"].cpu().numpy(), res.scores, ATOL, RTOL)[0]
-    assert close(outs[3]["hnew"].cpu().numpy(), res.hnew, ATOL, RTOL)[0]
+    assert close(outs[3]["scores"].cpu().numpy(), res.scores, *tol)[0]
+    assert close(outs[3]["hnew"].cpu().numpy(), res.hnew, *tol)[0]
