@@ -8,32 +8,35 @@ namespace rn {
 
 // k-significant-digit code of one fp32 element (Sec. 3 "rounding"), ties away
 // from zero. Code = sign<<15 | (e+20)<<10 | m for +-m*10^(e-k+1), zero -> 0.
-// |x| = M * 2^-s; the decade e = -j is found by comparing bit patterns with
-// the exact decade boundaries, then m = floor(M*10^p/2^s + 1/2) with
-// 10^p = 5^p * 2^p evaluated in 128-bit integers. Everything is computed in
-// registers: the boundaries are uniform (one comparison each, no per-lane
-// table index) and 5^p is a product of 5^(2^b) over the bits b of p.
+// |x| = M * 2^-s. Its decade j (10^-j <= |x| < 10^(1-j), i.e. j =
+// ceil(-log10 |x|)) is j1 = floor(n log10 2) + 1 or j1 + 1, where 2^-(n+1)
+// <= |x| < 2^-n; one exact comparison, M 5^j1 >= 2^(s-j1) in 128-bit
+// integers, decides. Then m = floor(M*10^p/2^s + 1/2) with 10^p = 5^p * 2^p,
+// p = k - 1 + j, from the same product. floor(n log10 2) is n * 1233 >> 12
+// for every n here (-1 .. 66). Everything is computed in registers: 5^j1 is
+// a product of 5^(2^b) over the bits b of j1, and the only table entry read
+// (10^-20, the smallest code) is uniform.
 __device__ __forceinline__ uint32_t sigdig_code(float x, int k, const DecadeTab &T, bool &bad) {
     uint32_t b = __float_as_uint(x);
     uint32_t neg = b >> 31, mag = b & 0x7FFFFFFFu;
     if (mag > 0x3F800000u) { bad = true; return 0u; }   // |x| > 1, inf, nan
     if (mag < T.lo[20]) return 0u;                       // |x| < 1e-20
-    // 10^-j <= |x| < 10^(1-j): the boundaries decrease with j, so j counts
-    // the boundaries above |x|
-    int j = 0;
-#pragma unroll
-    for (int c = 0; c < 20; ++c) j += mag < T.lo[c] ? 1 : 0;
-    uint32_t ex = mag >> 23;                             // normal: |x| >= 1e-20
-    u64 M = (u64)((mag & 0x7FFFFFu) | 0x800000u);
-    int s = 150 - (int)ex;
-    int p = k - 1 + j;                                   // 0 .. 22
-    u64 pow5 = (p & 1) ? 5ull : 1ull;
-    pow5 *= (p & 2) ? 25ull : 1ull;
-    pow5 *= (p & 4) ? 625ull : 1ull;
-    pow5 *= (p & 8) ? 390625ull : 1ull;
-    pow5 *= (p & 16) ? 152587890625ull : 1ull;
-    int sh = s - p;                                      // >= 18 for |x| <= 1
-    unsigned __int128 v = (unsigned __int128)M * pow5 + ((unsigned __int128)1 << (sh - 1));
+    const int ex = (int)(mag >> 23);                     // normal: |x| >= 1e-20
+    const u64 M = (u64)((mag & 0x7FFFFFu) | 0x800000u);
+    const int s = 150 - ex;
+    const int n = 126 - ex;                              // -1 .. 66
+    const int j1 = ((n * 1233) >> 12) + 1;               // 0 .. 20
+    u64 p5 = (j1 & 1) ? 5ull : 1ull;
+    p5 *= (j1 & 2) ? 25ull : 1ull;
+    p5 *= (j1 & 4) ? 625ull : 1ull;
+    p5 *= (j1 & 8) ? 390625ull : 1ull;
+    p5 *= (j1 & 16) ? 152587890625ull : 1ull;
+    const unsigned __int128 t = (unsigned __int128)M * p5;   // |x| 10^j1 = t 2^-(s - j1)
+    const bool ge = (t >> (s - j1)) != 0;                // |x| >= 10^-j1
+    const int j = ge ? j1 : j1 + 1;
+    const u64 f = (k == 1 ? 1ull : k == 2 ? 5ull : 25ull) * (ge ? 1ull : 5ull);   // 5^(p - j1)
+    const int sh = s - (k - 1 + j);                      // >= 18 for |x| <= 1
+    const unsigned __int128 v = t * f + ((unsigned __int128)1 << (sh - 1));
     uint32_t m = (uint32_t)(v >> sh);
     int e = -j;
     const uint32_t top = k == 1 ? 10u : k == 2 ? 100u : 1000u;   // 10^k
