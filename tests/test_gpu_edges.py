@@ -88,6 +88,22 @@ def test_planner_maximal_frame():
         b.frame(vec, words, qh, qt, tag="max %d" % t)
 
 
+def test_planner_round_boundaries():
+    """Frames on each side of the planner's per-thread round counts (1024
+    histories or queries per round of its 1024 threads; the launch sizes its
+    rounds to the frame): 1024 and 1025 histories, 1024, 1025, 2048, 2049,
+    4096 and 4097 queries, many equal keys of both kinds, the second frame
+    of each pair repeating the first's histories and queries."""
+    rng = np.random.default_rng(23)
+    b = Both(M, weights(M, rng), Q_SIGN, max_hist=1100, max_query=4200, cap_hist=1 << 13, cap_query=1 << 15)
+    for n_h, n_q in [(1024, 1024), (1025, 1025), (1024, 2048), (1025, 2049), (600, 4096), (1025, 4097)]:
+        vec, words, qh, qt = rand_frame(rng, M, n_h, n_q, dup_every=6)
+        qt = rng.integers(0, 60, n_q).astype(np.int32)   # few targets: many equal query keys
+        b.frame(vec, words, qh, qt, tag="%d/%d" % (n_h, n_q))
+        o2, r2 = b.frame(vec, words, qh, qt, tag="%d/%d again" % (n_h, n_q))
+        assert np.all(r2.h_status == HC_HIT), (n_h, n_q)
+
+
 def test_repeat_frame_hits_with_identical_bits():
     rng = np.random.default_rng(1)
     b = Both(M, weights(M, rng), Q_SIGDIG, 2)
