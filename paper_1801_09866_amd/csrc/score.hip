@@ -71,6 +71,12 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
     }
     float acc = 0.0f, me = 0.0f;
     if (!hit) {
+        // bias and MaxEnt weights: independent loads, issued with the rows
+        float mw[3];
+#pragma unroll
+        for (int o = 2; o <= 4; ++o)
+            mw[o - 2] = o <= d.me_order ? d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)] : 0.0f;
+        const float bo = d.b_out[t];
         const float *h = reinterpret_cast<const float *>(rec.hptr);
         if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
             const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
@@ -118,8 +124,10 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
                 acc = fmaf(__uint_as_float(a[st].w & 0xFFFF0000u), b1[st].w, acc);
             }
         }
-        me = d.b_out[t];
-        for (int o = 2; o <= d.me_order; ++o) me += d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)];
+        me = bo;   // the bias, then orders 2..N in turn
+        if (d.me_order >= 2) me += mw[0];
+        if (d.me_order >= 3) me += mw[1];
+        if (d.me_order >= 4) me += mw[2];
     }
     if (!hit) s = wave_sum(acc) + me;
     if (lane == 0) {
