@@ -34,7 +34,7 @@ __device__ __forceinline__ void stage_score(const Dev &d, long long e, int hs, i
     d.sc_stage[e] = en;
 }
 
-template <bool BF16>
+template <bool BF16, int RS>
 __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, int q, int lane, bool near_cap,
                                             int *s_cnt) {
     const QRec rec = d.f_qrec[q];
@@ -80,9 +80,9 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
         const float *h = reinterpret_cast<const float *>(rec.hptr);
         if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
             const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
-            float4 a[kRowSteps], b[kRowSteps];
+            float4 a[RS], b[RS];
 #pragma unroll
-            for (int st = 0; st < kRowSteps; ++st) {
+            for (int st = 0; st < RS; ++st) {
                 const int k = lane * 4 + st * 256;
                 a[st] = b[st] = make_float4(0.f, 0.f, 0.f, 0.f);
                 if (k < d.H) {
@@ -91,7 +91,7 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
                 }
             }
 #pragma unroll
-            for (int st = 0; st < kRowSteps; ++st) {
+            for (int st = 0; st < RS; ++st) {
                 acc = fmaf(a[st].x, b[st].x, acc);
                 acc = fmaf(a[st].y, b[st].y, acc);
                 acc = fmaf(a[st].z, b[st].z, acc);
@@ -99,10 +99,10 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
             }
         } else {   // 8 bf16 weights per lane per 512 elements
             const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
-            uint4 a[kRowSteps / 2];
-            float4 b0[kRowSteps / 2], b1[kRowSteps / 2];
+            uint4 a[RS / 2];
+            float4 b0[RS / 2], b1[RS / 2];
 #pragma unroll
-            for (int st = 0; st < kRowSteps / 2; ++st) {
+            for (int st = 0; st < RS / 2; ++st) {
                 const int k = lane * 8 + st * 512;
                 a[st] = make_uint4(0u, 0u, 0u, 0u);
                 b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -113,7 +113,7 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
                 }
             }
 #pragma unroll
-            for (int st = 0; st < kRowSteps / 2; ++st) {
+            for (int st = 0; st < RS / 2; ++st) {
                 acc = fmaf(__uint_as_float(a[st].x << 16), b0[st].x, acc);
                 acc = fmaf(__uint_as_float(a[st].x & 0xFFFF0000u), b0[st].y, acc);
                 acc = fmaf(__uint_as_float(a[st].y << 16), b0[st].z, acc);
@@ -145,6 +145,7 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
     }
 }
 
+template <int RS, int CS>
 __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f, int i, int lane) {
     // one round of loads: status, slot after the frame, where h' lives, and
     // the key's codes (needed if the key enters the cache)
@@ -152,23 +153,23 @@ __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f,
     const int slot = d.f_hslot[i];
     const float4 *src = reinterpret_cast<const float4 *>(d.f_hptr[i]);
     const bool enter = st == RNNLM_H_REP && slot >= 0;   // wave-uniform
-    u64 code[kCodeSteps];
+    u64 code[CS];
     if (enter) {
 #pragma unroll
-        for (int c = 0; c < kCodeSteps; ++c)
+        for (int c = 0; c < CS; ++c)
             if (lane + 64 * c < d.CW) code[c] = d.f_codes[(size_t)i * d.CW + lane + 64 * c];
     }
     // then the h' row, in flight while an admitted key enters the index
-    float4 v[kRowSteps];
+    float4 v[RS];
     if (f.hnew) {
 #pragma unroll
-        for (int k = 0; k < kRowSteps; ++k)
+        for (int k = 0; k < RS; ++k)
             if (lane + 64 * k < d.LH / 4) v[k] = ldg<float4>(src + lane + 64 * k);
     }
     if (enter) {
         u64 *dst = d.hc_codes + (size_t)slot * d.CW;
 #pragma unroll
-        for (int c = 0; c < kCodeSteps; ++c)
+        for (int c = 0; c < CS; ++c)
             if (lane + 64 * c < d.CW) dst[lane + 64 * c] = code[c];
         if (lane == 0) {
             const HistRec hr = d.f_hrec[i];
@@ -187,7 +188,7 @@ __device__ __forceinline__ void finish_history(const Dev &d, const FrameArgs &f,
     if (f.hnew) {
         float4 *dst = reinterpret_cast<float4 *>(f.hnew + (size_t)i * d.LH);
 #pragma unroll
-        for (int k = 0; k < kRowSteps; ++k)
+        for (int k = 0; k < RS; ++k)
             if (lane + 64 * k < d.LH / 4) dst[lane + 64 * k] = v[k];
     }
 }
@@ -249,7 +250,7 @@ __device__ void admit_in_order(const Dev &d, const FrameArgs &f, int *s_tmp) {
 // Each frame of the launch owns a contiguous range of blocks: its query
 // blocks, then its history blocks. MULTI = false: one frame, whose range is
 // the whole grid (everything at fixed argument offsets).
-template <bool BF16, bool MULTI>
+template <bool BF16, bool MULTI, int RS, int CS>
 __global__ __launch_bounds__(256) void k_score_finish(Dev d0, FrameBlock fb) {
     __shared__ int s_cnt[4];
     __shared__ int s_tmp[8];
@@ -266,10 +267,10 @@ __global__ __launch_bounds__(256) void k_score_finish(Dev d0, FrameBlock fb) {
     __syncthreads();
     if (b < qblocks) {
         const int q = b * 4 + w;
-        if (q < f.n_query) score_query<BF16>(d, f, q, lane, near_cap, s_cnt);
+        if (q < f.n_query) score_query<BF16, RS>(d, f, q, lane, near_cap, s_cnt);
     } else {
         const int i = (b - qblocks) * 4 + w;
-        if (i < f.n_hist) finish_history(d, f, i, lane);
+        if (i < f.n_hist) finish_history<RS, CS>(d, f, i, lane);
     }
     __syncthreads();
     if (tid == 0 && b < qblocks)   // folded into the counters by the next keys kernel
@@ -286,16 +287,29 @@ __global__ __launch_bounds__(256) void k_score_finish(Dev d0, FrameBlock fb) {
     if (tid == 0) d.ctr[C_DONE] = 0;
 }
 
-void launch_score_finish(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts) {
+template <int RS, int CS>
+static void launch_sf(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts) {
     const int nb = fb.boff[fb.n];
     const bool multi = fb.n > 1;
     if (d.wdtype == RNNLM_BF16) {
-        if (multi) launch_k(k_score_finish<true, true>, nb, 256, s, ts, d, fb);
-        else launch_k(k_score_finish<true, false>, nb, 256, s, ts, d, fb);
+        if (multi) launch_k(k_score_finish<true, true, RS, CS>, nb, 256, s, ts, d, fb);
+        else launch_k(k_score_finish<true, false, RS, CS>, nb, 256, s, ts, d, fb);
     } else {
-        if (multi) launch_k(k_score_finish<false, true>, nb, 256, s, ts, d, fb);
-        else launch_k(k_score_finish<false, false>, nb, 256, s, ts, d, fb);
+        if (multi) launch_k(k_score_finish<false, true, RS, CS>, nb, 256, s, ts, d, fb);
+        else launch_k(k_score_finish<false, false, RS, CS>, nb, 256, s, ts, d, fb);
     }
+}
+
+// Register arrays sized to the model: with rows of at most 1024 elements and
+// keys of at most 256 code words a wave holds half the row registers and a
+// quarter of the code registers of the longest case, and eight waves fit per
+// SIMD instead of six or seven.
+void launch_score_finish(const Dev &d, const FrameBlock &fb, hipStream_t s, Stamp ts) {
+    const bool short_row = d.LH <= 1024, short_key = d.CW <= 256;
+    if (short_row && short_key) launch_sf<4, 4>(d, fb, s, ts);
+    else if (short_row) launch_sf<4, kCodeSteps>(d, fb, s, ts);
+    else if (short_key) launch_sf<kRowSteps, 4>(d, fb, s, ts);
+    else launch_sf<kRowSteps, kCodeSteps>(d, fb, s, ts);
 }
 
 }  // namespace rn

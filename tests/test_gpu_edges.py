@@ -155,6 +155,22 @@ def test_two_layer_fp32_and_exact_mode():
         b.frame(*rand_frame(rng, m, 70, 400, dup_every=4), tag="L2 %d" % t)
 
 
+@pytest.mark.parametrize("L,H,qmode,k", [(1, 512, Q_SIGN, 0), (1, 1024, Q_SIGDIG, 2), (1, 1024, Q_EXACT, 0),
+                                         (2, 576, Q_SIGN, 0), (2, 576, Q_SIGDIG, 2), (2, 1024, Q_EXACT, 0)],
+                         ids=["LH512-sign", "LH1024-sigdig2-cw256", "LH1024-exact-cw512", "LH1152-sign",
+                              "LH1152-sigdig2-cw288", "LH2048-exact-cw1024"])
+def test_scorer_register_sizes(L, H, qmode, k):
+    """The scoring kernel holds a row of at most 1024 elements and a key of
+    at most 256 code words in fewer registers; every combination of short or
+    long rows and keys, at both limits, against the oracle."""
+    m = ModelCfg(V=3000, E=64, H=H, L=L, wdtype=F32, maxent_log2=12, maxent_order=4)
+    rng = np.random.default_rng(40 + L * 7 + H + qmode)
+    b = Both(m, weights(m, rng), qmode, k, max_hist=64, max_query=512)
+    frames = [rand_frame(rng, m, 48, 300, dup_every=5) for _ in range(2)]
+    for t, f in enumerate(frames + frames[:1]):   # the repeat: cache hits and stored scores
+        b.frame(*f, tag="L%d H%d %d" % (L, H, t))
+
+
 def test_device_errors_are_sticky_until_reset():
     rng = np.random.default_rng(6)
     g = R.Scorer(M, weights(M, rng), Q_SIGDIG, 2, max_hist=64, max_query=64)
