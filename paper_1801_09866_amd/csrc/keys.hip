@@ -55,18 +55,18 @@ __device__ __forceinline__ bool nonfinite(float x) {
 }
 
 // ---------------------------------------------------------------------------
-// K1: one wave per history: validate, quantise into code words, hash the key
-// (codes, GRU input word), and probe the history cache with an exact code
-// comparison. Each lane keeps its code words in registers:
+// K1: one wave per history (sign and exact keys; k significant digits take a
+// block per history, below): validate, quantise into code words, hash the
+// key (codes, GRU input word), and probe the history cache with an exact
+// code comparison. Each lane keeps its code words in registers:
 //   SIGN   word w (64 elements, one ballot) is held by lane w      (CW <= 32)
-//   SIGDIG word w = elements 4w..4w+3, held by lane w % 64, slot w / 64
 //   EXACT  word w = elements 2w, 2w+1, held by lane w % 64, slot w / 64
 // ---------------------------------------------------------------------------
 constexpr int kWordsPerLane = kMaxCW / 64;   // 16
 constexpr int kSignWords = kMaxLH / 64;      // sign code words of the longest vector
 
 // Block roles (independent work, so one launch runs them side by side):
-//   [0, hb)            one wave per history (below)
+//   [0, hb)            one wave per history, or one block for k significant digits
 //   [hb, hb+qb)        one thread per query: its key, validated
 //   [hb+qb, hb+qb+sb)  enter the scores the previous frame admitted into the
 //                      LM-query cache
@@ -129,7 +129,7 @@ __device__ void fold_counts(const Dev &d, int npart) {
 // the wave also writes the row's bf16 copy (fp32 models keep no row elements
 // live across the cache probe, and more waves fit).
 template <bool BF16>
-__device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, int i) {
+__device__ void hist_wave(const Dev &d, const FrameArgs &f, int i) {
     const int lane = threadIdx.x & 63;
     if (i >= f.n_hist) return;
     // the record's words are loaded with the row, not after it
@@ -143,8 +143,8 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
     bool bad = false;
     u64 hs = 0;
     // the lane's row elements, kept for the GEMM's bf16 copy of the row:
-    // sign v[u] = element 64 u + lane; k digits float4 s = elements
-    // 4 (lane + 64 s) ..; exact float2 s = elements 2 (lane + 64 s) ..
+    // sign v[u] = element 64 u + lane; exact float2 s = elements
+    // 2 (lane + 64 s) ..
     static_assert(kSignWords <= 32 && 2 * kWordsPerLane <= 32, "row elements per lane");
     __attribute__((aligned(16))) float rv[32];   // registers: indexed only by constants
     if (d.qmode == RNNLM_Q_SIGN) {
@@ -163,23 +163,6 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
             }
         }
         if (lane < CW) hs = mix64(words[0] ^ ((u64)(lane + 1) * kPhi));
-    } else if (d.qmode == RNNLM_Q_SIGDIG) {
-        // all of the row's loads first (4 elements per code word), then the codes
-        float4 *v = reinterpret_cast<float4 *>(rv);
-#pragma unroll
-        for (int s = 0; s < kWordsPerLane / 2; ++s)
-            v[s] = lane + 64 * s < CW ? ldg<float4>(x + 4 * (lane + 64 * s)) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int s = 0; s < kWordsPerLane / 2; ++s) {
-            const int w = lane + 64 * s;
-            if (w < CW) {
-                words[s] = (u64)sigdig_code(v[s].x, d.qdigits, T, bad) |
-                           ((u64)sigdig_code(v[s].y, d.qdigits, T, bad) << 16) |
-                           ((u64)sigdig_code(v[s].z, d.qdigits, T, bad) << 32) |
-                           ((u64)sigdig_code(v[s].w, d.qdigits, T, bad) << 48);
-                hs += mix64(words[s] ^ ((u64)(w + 1) * kPhi));
-            }
-        }
     } else {
         // all of the row's loads first (2 elements per code word), then the codes
         float2 *v = reinterpret_cast<float2 *>(rv);
@@ -246,12 +229,6 @@ __device__ void hist_wave(const Dev &d, const FrameArgs &f, const DecadeTab &T, 
 #pragma unroll
             for (int u = 0; u < kSignWords; ++u)
                 if (u < CW) hb[u * 64 + lane] = f32_to_bf16(rv[u]);
-        } else if (d.qmode == RNNLM_Q_SIGDIG) {
-            uint2 *hb = reinterpret_cast<uint2 *>(d.f_hbf + (size_t)i * d.LH);
-            const float4 *v = reinterpret_cast<const float4 *>(rv);
-#pragma unroll
-            for (int s = 0; s < kWordsPerLane / 2; ++s)
-                if (lane + 64 * s < CW) hb[lane + 64 * s] = pack_bf16x4(v[s]);
         } else {
             uint32_t *hb = reinterpret_cast<uint32_t *>(d.f_hbf + (size_t)i * d.LH);
             const float2 *v = reinterpret_cast<const float2 *>(rv);
@@ -424,7 +401,7 @@ __global__ __launch_bounds__(256) void k_hist_key(Dev d0, FrameBlock fb, DecadeT
     const FrameArgs &f = fb.f[e];
     if (role == 0) {
         if (d.qmode == RNNLM_Q_SIGDIG) hist_block_sigdig(d, f, T, lb);   // one block per history
-        else hist_wave<BF16>(d, f, T, lb * 4 + wave_id());              // one wave per history
+        else hist_wave<BF16>(d, f, lb * 4 + wave_id());                 // one wave per history
     }
     else if (role == 1) query_key(d, f, lb * blockDim.x + threadIdx.x);
     else if (role == 2) insert_staged(d, lb, fb.soff[e + 1] - fb.soff[e]);
