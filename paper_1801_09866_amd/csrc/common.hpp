@@ -210,10 +210,6 @@ __device__ __forceinline__ u64 mix64(u64 z) {
     return z ^ (z >> 31);
 }
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
-    return __uint_as_float(((uint32_t)b) << 16);
-}
-
 // round-to-nearest-even fp32 -> bf16 (inputs are finite)
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     uint32_t u = __float_as_uint(f);

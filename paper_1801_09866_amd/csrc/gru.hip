@@ -113,39 +113,6 @@ __device__ __forceinline__ RowSrc row_source(const Dev &d, const Rows &R, int la
     return r;
 }
 
-__device__ __forceinline__ void gru_epilogue(const Dev &d, const Rows &R, int layer, int M, int m0,
-                                             int j0, int rb, int ub, const f4_t &ar, const f4_t &az,
-                                             const f4_t &anx, const f4_t &anh) {
-    const int lane = threadIdx.x & 63;
-    const int j = j0 + ub * 16 + (lane & 15);
-    const float *b = d.bl;
-    const float br = b[j], bz = b[d.H + j], bn = b[2 * d.H + j];
-    // every load first (the stores could alias them as far as the compiler
-    // knows, which would serialise one round trip per row)
-    int mrow[4];
-    const float *src[4];
-    float *dst[4];
-    float hprev[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        mrow[e] = m0 + rb * 16 + 4 * (lane >> 4) + e;
-        const bool ok = mrow[e] < M;
-        src[e] = ok ? reinterpret_cast<const float *>(row_at(R, d.f_rowh, mrow[e])) : nullptr;
-        dst[e] = ok ? reinterpret_cast<float *>(row_at(R, d.f_rowdst, mrow[e])) : nullptr;
-    }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) hprev[e] = mrow[e] < M ? src[e][(size_t)layer * d.H + j] : 0.0f;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        if (mrow[e] < M) {
-            const float r = sigmoidf_(ar[e] + br);
-            const float z = sigmoidf_(az[e] + bz);
-            const float n = tanhf(anx[e] + bn + r * anh[e]);
-            dst[e][(size_t)layer * d.H + j] = (1.0f - z) * n + z * hprev[e];
-        }
-    }
-}
-
 __device__ __forceinline__ uint4 pack_bf16x8(float4 a, float4 b) {
     uint4 r;
     r.x = (uint32_t)f32_to_bf16(a.x) | ((uint32_t)f32_to_bf16(a.y) << 16);
