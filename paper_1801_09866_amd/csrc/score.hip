@@ -78,24 +78,32 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
             mw[o - 2] = o <= d.me_order ? d.maxent[maxent_slot(o, w1, key.y, key.z, t, d.me_log2)] : 0.0f;
         const float bo = d.b_out[t];
         const float *h = reinterpret_cast<const float *>(rec.hptr);
+        // The row loads are unconditional (a lane past the row reads its
+        // start and its terms are zeroed in the sum): guarded loads become
+        // separate blocks, after which the compiler waits for the first
+        // step's data before it issues the next step's loads.
         if (!BF16) {   // the whole row in flight: 16 B per lane per 256 elements
             const float *u = reinterpret_cast<const float *>(d.U_out) + (size_t)t * d.H;
             float4 a[RS], b[RS];
 #pragma unroll
             for (int st = 0; st < RS; ++st) {
                 const int k = lane * 4 + st * 256;
+                const int kc = k < d.H ? k : 0;
                 a[st] = b[st] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (k < d.H) {
-                    a[st] = ldg<float4>(u + k);
-                    b[st] = ldg<float4>(h + k);
+                if (st < 4 || d.H > 1024) {   // wave-uniform: rows past 1024 elements only
+                    a[st] = ldg<float4>(u + kc);
+                    b[st] = ldg<float4>(h + kc);
                 }
             }
+            const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
             for (int st = 0; st < RS; ++st) {
-                acc = fmaf(a[st].x, b[st].x, acc);
-                acc = fmaf(a[st].y, b[st].y, acc);
-                acc = fmaf(a[st].z, b[st].z, acc);
-                acc = fmaf(a[st].w, b[st].w, acc);
+                const bool in = lane * 4 + st * 256 < d.H;
+                const float4 x = in ? a[st] : z4, y = in ? b[st] : z4;
+                acc = fmaf(x.x, y.x, acc);
+                acc = fmaf(x.y, y.y, acc);
+                acc = fmaf(x.z, y.z, acc);
+                acc = fmaf(x.w, y.w, acc);
             }
         } else {   // 8 bf16 weights per lane per 512 elements
             const uint16_t *u = reinterpret_cast<const uint16_t *>(d.U_out) + (size_t)t * d.H;
@@ -104,16 +112,21 @@ __device__ __forceinline__ void score_query(const Dev &d, const FrameArgs &f, in
 #pragma unroll
             for (int st = 0; st < RS / 2; ++st) {
                 const int k = lane * 8 + st * 512;
+                const int kc = k < d.H ? k : 0;
                 a[st] = make_uint4(0u, 0u, 0u, 0u);
                 b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (k < d.H) {
-                    a[st] = ldg<uint4>(u + k);
-                    b0[st] = ldg<float4>(h + k);
-                    b1[st] = ldg<float4>(h + k + 4);
+                if (st < 2 || d.H > 1024) {   // wave-uniform: rows past 1024 elements only
+                    a[st] = ldg<uint4>(u + kc);
+                    b0[st] = ldg<float4>(h + kc);
+                    b1[st] = ldg<float4>(h + kc + 4);
                 }
             }
 #pragma unroll
             for (int st = 0; st < RS / 2; ++st) {
+                if (lane * 8 + st * 512 >= d.H) {   // terms past the row are zero
+                    a[st] = make_uint4(0u, 0u, 0u, 0u);
+                    b0[st] = b1[st] = make_float4(0.f, 0.f, 0.f, 0.f);
+                }
                 acc = fmaf(__uint_as_float(a[st].x << 16), b0[st].x, acc);
                 acc = fmaf(__uint_as_float(a[st].x & 0xFFFF0000u), b0[st].y, acc);
                 acc = fmaf(__uint_as_float(a[st].y << 16), b0[st].z, acc);

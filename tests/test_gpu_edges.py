@@ -29,6 +29,10 @@ def weights(m, rng, scale=0.05):
 
 class Both:
     def __init__(self, m, w, qmode, k=0, max_hist=300, max_query=3000, cap_hist=1 << 12, cap_query=1 << 14):
+        # h' is a GRU step over K = E + H terms in fp32; the fixed bar holds
+        # for the configurations' K <= 1536, and the rounding error of a
+        # K-term sum grows with K, so longer sums scale the absolute bar
+        self.hatol = ATOL * max(1.0, max(m.E + m.H, 2 * m.H if m.L == 2 else 0) / 1536)
         self.o = Oracle(m.V, m.E, m.H, m.L, m.maxent_log2, m.maxent_order, w, qmode, k,
                         cap_hist=cap_hist, cap_query=cap_query, seed=R.DEFAULT_SEED)
         self.g = R.Scorer(m, w, qmode, k, max_hist=max_hist, max_query=max_query,
@@ -45,7 +49,9 @@ class Both:
         assert np.array_equal(out["h_hash"][:n_h].cpu().numpy().view(np.uint64), res.h_hash), tag
         assert np.array_equal(out["h_status"][:n_h].cpu().numpy(), res.h_status), tag
         assert np.array_equal(out["h_rep"][:n_h].cpu().numpy(), res.h_rep), tag
-        assert close(out["hnew"][:n_h].cpu().numpy(), res.hnew, ATOL, RTOL)[0], tag
+        g, w = out["hnew"][:n_h].cpu().numpy().astype(np.float64), res.hnew
+        ok, emax = close(g, w, self.hatol, RTOL)
+        assert ok, (tag, "h' max error %.3g, %.3f of the tolerance" % (emax, (np.abs(g - w) / (self.hatol + RTOL * np.abs(w))).max()))
         if n_q:
             assert np.array_equal(out["q_status"][:n_q].cpu().numpy(), res.q_status), tag
             assert np.array_equal(out["q_rep"][:n_q].cpu().numpy(), res.q_rep), tag
@@ -156,13 +162,16 @@ def test_two_layer_fp32_and_exact_mode():
 
 
 @pytest.mark.parametrize("L,H,qmode,k", [(1, 512, Q_SIGN, 0), (1, 1024, Q_SIGDIG, 2), (1, 1024, Q_EXACT, 0),
-                                         (2, 576, Q_SIGN, 0), (2, 576, Q_SIGDIG, 2), (2, 1024, Q_EXACT, 0)],
+                                         (2, 576, Q_SIGN, 0), (2, 576, Q_SIGDIG, 2), (2, 1024, Q_EXACT, 0),
+                                         (1, 1088, Q_SIGN, 0), (1, 2048, Q_SIGN, 0)],
                          ids=["LH512-sign", "LH1024-sigdig2-cw256", "LH1024-exact-cw512", "LH1152-sign",
-                              "LH1152-sigdig2-cw288", "LH2048-exact-cw1024"])
+                              "LH1152-sigdig2-cw288", "LH2048-exact-cw1024", "H1088-sign", "H2048-sign"])
 def test_scorer_register_sizes(L, H, qmode, k):
     """The scoring kernel holds a row of at most 1024 elements and a key of
     at most 256 code words in fewer registers; every combination of short or
-    long rows and keys, at both limits, against the oracle."""
+    long rows and keys, at both limits, against the oracle. Output rows
+    longer than 1024 elements (H = 1088: only some lanes of the fifth step
+    are inside the row; H = 2048: every step) take the upper load steps."""
     m = ModelCfg(V=3000, E=64, H=H, L=L, wdtype=F32, maxent_log2=12, maxent_order=4)
     rng = np.random.default_rng(40 + L * 7 + H + qmode)
     b = Both(m, weights(m, rng), qmode, k, max_hist=64, max_query=512)
